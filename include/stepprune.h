@@ -1,0 +1,198 @@
+/*
+ * stepprune.h -- C ABI of the StepPrune inference-time selection library for
+ * AMD MI355X (gfx950).
+ *
+ * The library runs the three stages of the paper's inference procedure
+ * (Algorithm 1):
+ *   stepprune_project  step 1: project visual tokens, START/STOP embeddings and
+ *                      the text context once (Section "Conditional Sequential
+ *                      Pointer Policy": text projection, LayerNorm, gain g_text;
+ *                      the pointer decoder's key/query/value projections);
+ *   stepprune_select   steps 2-4: the sequential pointer policy with STOP (Eq. 2,
+ *                      Eq. 4), every group of every image run as an independent
+ *                      episode, kept indices restored to native order;
+ *   stepprune_compact  step 5: physical gather of the kept tokens ahead of the
+ *                      prompt into a padded or packed prefill buffer.
+ *
+ * Conventions shared by every call
+ *  - Pointers are DEVICE pointers unless marked (host).  All row-major.
+ *  - Rows of visual tokens of all images are packed back to back; image b owns
+ *    rows [img_off[b], img_off[b+1]).  Indices in the outputs are image-local.
+ *  - Every call validates its host-side arguments first and returns a status
+ *    before launching anything.  On SP_OK the work is enqueued on `stream` and
+ *    the call returns; outputs are valid once the stream has been synchronised.
+ *  - The library allocates no memory and keeps no state besides kernel handles.
+ *    The caller owns every buffer, including the workspace `ws` whose size
+ *    stepprune_workspace_bytes() gives; a workspace may be reused by later calls
+ *    on the same stream.
+ *  - Errors that depend on device-resident data (inconsistent offsets, a group
+ *    larger than the stated maximum, counts that do not fit the output) are
+ *    recorded in a device error word inside `ws`; the affected outputs are
+ *    then undefined.  stepprune_read_device_error() reads it.
+ *  - No C++ exception crosses this interface.
+ *
+ * Numerics: projections accumulate in float32 and are stored once, rounded to
+ * nearest-even, in the dtype of sp_dims (bfloat16 or float32); the text context
+ * and all selection arithmetic are float32.  sigma = h^(-1/2) is applied to the
+ * history-attention scores and to the pointer logits; the STOP bias b_stop is
+ * added to the STOP logit unscaled.  Exact ties go to the lowest token index and
+ * STOP loses ties against tokens (it is last in the candidate memory).
+ */
+#ifndef STEPPRUNE_H
+#define STEPPRUNE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SP_OK = 0,
+  SP_EINVAL = 1,        /* a host-side argument is invalid (null, size, alignment) */
+  SP_EUNSUPPORTED = 2,  /* valid but not supported by this build (dtype, g > 1, sizes) */
+  SP_EWORKSPACE = 3,    /* ws_bytes smaller than stepprune_workspace_bytes() */
+  SP_EHIP = 4,          /* a HIP launch or runtime call failed */
+  SP_EDEVICE = 5        /* the device error word is set (read_device_error) */
+} sp_status;
+
+typedef enum { SP_F32 = 0, SP_BF16 = 1 } sp_dtype;
+
+enum {
+  SP_TRACE = 1u,       /* stepprune_select writes the per-step trace */
+  SP_NO_HISTORY = 2u   /* pointer query frozen at its first value (diagnostic:
+                          the selector collapses to top-K of the first scores, Eq. 1) */
+};
+
+enum { SP_LAYOUT_PADDED = 0, SP_LAYOUT_PACKED = 1 };
+
+/* Device error word values (stepprune_read_device_error). */
+enum {
+  SP_DEV_OK = 0,
+  SP_DEV_BAD_OFFSETS = 1,   /* an offset array is not non-decreasing or exceeds its total */
+  SP_DEV_GROUP_TOO_LARGE = 2,/* a group has more tokens than max_group */
+  SP_DEV_BAD_CAP = 3,       /* a group cap is negative or exceeds max_cap */
+  SP_DEV_OUTPUT_OVERFLOW = 4 /* kept or prefill rows exceed the capacity given */
+};
+
+/* Shapes shared by the calls (host). d, d_text and h are multiples of 64,
+   h <= 1024 (h <= 512 for SP_F32).  dtype applies to X, E_text, s_start,
+   s_stop, W_kqv, W_text, KQV and the compaction output. */
+typedef struct {
+  int32_t d;        /* visual feature width */
+  int32_t d_text;   /* text embedding width */
+  int32_t h;        /* selector hidden width */
+  int32_t dtype;    /* sp_dtype */
+} sp_dims;
+
+/*
+ * Algorithm 1 step 1.  Projects every visual row and the START and STOP
+ * embeddings with one weight matrix, and pools the text context per image.
+ *
+ *  X        [T_vis, d]        visual tokens of all images, packed
+ *  s_start  [d], s_stop [d]   learned START / STOP embeddings
+ *  W_kqv    [3h, d]           output-major: rows [0,h) key, [h,2h) query,
+ *                             [2h,3h) value features (x -> x W_kqv^T)
+ *  E_text   [T_txt, d_text]   text embeddings of all images, packed by
+ *  text_off [B+1]             text_off (device); T_txt = text_off[B] (host copy)
+ *  W_text   [h, d_text]       text projection into the pointer query space
+ *  g_text, ln_eps             c_b = g_text * mean_l LN(E_{b,l} W_text^T),
+ *                             LayerNorm without affine, biased variance;
+ *                             an image without text gets c_b = 0
+ *  KQV      out [T_vis+2, 3h] row T_vis = START, row T_vis+1 = STOP
+ *  ctx      out [B, h] float32
+ *  ws       workspace of stepprune_workspace_bytes(0, ...)
+ */
+sp_status stepprune_project(const sp_dims* dims,
+                            const void* X, int64_t T_vis,
+                            const void* s_start, const void* s_stop,
+                            const void* W_kqv,
+                            const void* E_text, const int32_t* text_off,
+                            int32_t B, int64_t T_txt,
+                            const void* W_text, float g_text, float ln_eps,
+                            void* KQV, float* ctx,
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Algorithm 1 steps 2-4 (Eq. 2, Eq. 4).  Every group (a contiguous run of one
+ * image's visual rows) is an independent episode: history [START], then per
+ * round t = 1..cap the pointer query
+ *     u_t = c_b + q_e + sum_tau softmax_tau(sigma <q_e, k_tau>) v_tau
+ * (e the newest history entry, tau over the history), logits
+ * l_t(j) = sigma <u_t, k_j> over the group's unselected tokens and
+ * l_t(STOP) = sigma <u_t, k_stop> + b_stop; the first maximal candidate is
+ * taken; STOP ends the episode; a token is masked and appended to the history.
+ * At the cap the episode ends without a STOP step.
+ *
+ *  KQV, ctx       outputs of stepprune_project (T_vis visual rows + START + STOP)
+ *  img_off [B+1]  visual row offsets per image
+ *  grp_off [G+1]  visual row offsets per group; groups of an image are
+ *                 contiguous and in row order, grp_img [G] their image,
+ *                 grp_cap [G] their round cap (>= 0)
+ *  max_group      (host) upper bound on any group's size, <= 1022
+ *  max_cap        (host) upper bound on any group's effective cap min(cap, n)
+ *  kept_off [B+1] offsets of each image's slice of kept_idx; the slice must
+ *                 hold sum over its groups of min(cap, n)
+ *  b_stop         additive STOP bias (may be +-inf)
+ *  g              tokens kept per non-STOP round; only g = 1 is supported
+ *  flags          SP_TRACE, SP_NO_HISTORY
+ *  kept_idx  out  image-local kept indices, ascending per image, at kept_off[b]
+ *  kept_cnt  out  [B] kept count per image
+ *  grp_cnt   out  [G] kept count per group, or NULL
+ *  trace     out  with SP_TRACE: [G, trace_steps, 4] float32 records per step:
+ *                 {taken candidate (int32 bits; -1 = STOP), its logit,
+ *                  the runner-up candidate logit (-inf if none), STOP logit};
+ *                 steps past the end hold taken = -2.  NULL otherwise.
+ */
+sp_status stepprune_select(const sp_dims* dims,
+                           const void* KQV, const float* ctx, int64_t T_vis,
+                           const int32_t* img_off, int32_t B,
+                           const int32_t* grp_off, const int32_t* grp_img,
+                           const int32_t* grp_cap, int32_t G,
+                           int32_t max_group, int32_t max_cap,
+                           const int32_t* kept_off,
+                           float b_stop, int32_t g, uint32_t flags,
+                           int32_t* kept_idx, int32_t* kept_cnt, int32_t* grp_cnt,
+                           float* trace, int32_t trace_steps,
+                           void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Algorithm 1 step 5.  Gathers each image's kept visual rows (ascending) and
+ * then its text rows into the prefill buffer.  Requires d_text == d.
+ *
+ *  layout SP_LAYOUT_PADDED: image b owns out rows [b*rows_per_image,
+ *         (b+1)*rows_per_image); rows past K_b + L_b are left untouched;
+ *         seq_info [B] = K_b + L_b.
+ *  layout SP_LAYOUT_PACKED: sequences back to back; seq_info [B+1] =
+ *         cu_seqlens, cu[0] = 0, cu[b+1] = cu[b] + K_b + L_b; rows_per_image
+ *         is ignored.
+ *  out_rows (host) rows of `out`; writes beyond it set SP_DEV_OUTPUT_OVERFLOW.
+ */
+sp_status stepprune_compact(const sp_dims* dims,
+                            const void* X, const int32_t* img_off,
+                            const void* E_text, const int32_t* text_off,
+                            const int32_t* kept_idx, const int32_t* kept_off,
+                            const int32_t* kept_cnt, int32_t B,
+                            int32_t layout, int32_t rows_per_image, int64_t out_rows,
+                            void* out, int32_t* seq_info,
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Workspace bytes for stage `which` (0 project, 1 select, 2 compact) at the
+   given sizes (host).  Returns 0 for invalid arguments. */
+size_t stepprune_workspace_bytes(int32_t which, const sp_dims* dims, int64_t T_vis,
+                                 int64_t T_txt, int32_t B, int32_t G,
+                                 int32_t max_group, int32_t max_cap);
+
+/* Synchronises `stream`, then copies the device error word of `ws` to *code
+   (host) and clears it.  Returns SP_EDEVICE if it was set. */
+sp_status stepprune_read_device_error(void* ws, hipStream_t stream, int32_t* code);
+
+/* Static description of a status code. */
+const char* stepprune_status_string(sp_status status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* STEPPRUNE_H */

@@ -1,0 +1,438 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test names the passage or fact it rests on.  None of them compares the
+oracle with a retyping of its own formulas: they use hand-worked episodes,
+library routines (torch attention, matmul, layer_norm, topk, bfloat16
+conversion), brute-force enumeration, and invariants of the method.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.selection import STOP
+from paper_2609_13804_amd import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "worked_examples.json")
+
+
+def _examples():
+    with open(GOLDEN) as f:
+        return json.load(f)["examples"]
+
+
+def _run_example(ex):
+    h = ex["h"]
+    zero = np.zeros(h)
+    return oracle.run_episode(np.array(ex["K"], float), np.array(ex["Q"], float),
+                              np.array(ex["V"], float), (zero, zero, zero),
+                              np.array(ex["k_stop"], float), np.array(ex["c"], float),
+                              ex["cap"], ex["b_stop"], h, no_history=ex["no_history"])
+
+
+# ---------------------------------------------------------------- worked examples
+
+@pytest.mark.parametrize("ex", _examples(), ids=lambda e: e["name"])
+def test_worked_example(ex):
+    """Hand-worked episodes (tests/golden/worked_examples.json)."""
+    res = _run_example(ex)
+    assert res.actions == ex["actions"]
+    assert res.stopped == ex["stopped"]
+    assert len(res.steps) == len(ex["logits"])
+    for step, want, want_stop in zip(res.steps, ex["logits"], ex["stop_logits"]):
+        got = step.logits
+        for g, w in zip(got, want):
+            if w is None:
+                assert g == -np.inf
+            else:
+                assert abs(g - w) <= 1e-12
+        assert abs(step.stop_logit - want_stop) <= 1e-12
+
+
+# ---------------------------------------------------------------- rounding
+
+def test_bf16_rounding_matches_torch_conversion():
+    """Round-to-nearest-even to bfloat16 agrees with torch's float32 -> bfloat16
+    conversion on float32-exact inputs over the whole exponent range."""
+    rng = np.random.default_rng(7)
+    x = rng.standard_normal(400_000) * np.exp2(rng.integers(-140, 126, 400_000))
+    x = x.astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).double().numpy()
+    got = oracle.round_bf16(x.astype(np.float64))
+    same = (got == ref) | (np.isnan(got) & np.isnan(ref))
+    assert same.all()
+
+
+def test_bf16_rounding_ties_and_edges():
+    """Halfway cases go to the even neighbour; overflow gives inf; zero, inf and
+    NaN pass through (bfloat16 format: 8 significant bits, float32 range)."""
+    cases = {
+        1 + 2 ** -8: 1.0,                 # halfway between 1 and 1+2^-7: even is 1
+        1 + 3 * 2 ** -8: 1 + 2 ** -6,     # halfway between 1+2^-7 and 1+2^-6: even is 1+2^-6
+        1 + 2 ** -8 + 2 ** -40: 1 + 2 ** -7,
+        -(1 + 2 ** -8): -1.0,
+        255.5: 256.0,
+        2.0 ** 128 - 2.0 ** 119: math.inf,
+        2.0 ** -133: 2.0 ** -133,         # smallest subnormal
+        2.0 ** -134: 0.0,                 # half of it: ties to even (zero)
+        3 * 2.0 ** -134: 2.0 ** -132,
+        0.0: 0.0,
+    }
+    got = oracle.round_bf16(np.array(list(cases.keys())))
+    assert list(got) == list(cases.values())
+    assert np.isnan(oracle.round_bf16(np.array([np.nan]))[0])
+
+
+def test_f32_rounding_is_numpy_cast():
+    x = np.array([1 + 2 ** -24, 1 + 3 * 2 ** -24, 0.1])
+    assert list(oracle.round_f32(x)) == [1.0, 1 + 2 ** -22, float(np.float32(0.1))]
+
+
+# ---------------------------------------------------------------- projection
+
+def test_projection_matches_library_matmul():
+    """Algorithm 1 step 1: the projected rows are the exact product (torch fp64
+    matmul as the library reference) rounded once to the storage dtype."""
+    rng = np.random.default_rng(3)
+    d, h, n = 96, 32, 37
+    X = rng.standard_normal((n, d))
+    s0, s1 = rng.standard_normal(d), rng.standard_normal(d)
+    Wk = rng.standard_normal((3 * h, d)) / math.sqrt(d)
+    for dtype in ("f32", "bf16"):
+        KQV = oracle.project(X, s0, s1, Wk, dtype)
+        Xa = torch.from_numpy(np.vstack([X, s0, s1]))
+        ref = torch.matmul(Xa, torch.from_numpy(Wk).t())
+        if dtype == "f32":
+            ref = ref.float().double()
+        else:
+            ref = ref.float().to(torch.bfloat16).double()   # ref via fp32: allow 1-ulp double-rounding flips
+        diff = np.abs(KQV - ref.numpy())
+        ulp = np.abs(ref.numpy()) * (2.0 ** -7 if dtype == "bf16" else 2.0 ** -23)
+        assert (diff <= ulp + 1e-300).all()
+        assert KQV.shape == (n + 2, 3 * h)
+
+
+def test_text_context_matches_torch_layer_norm():
+    """c_b = g_text * mean_l LN(E_{b,l} W^T) with torch's layer_norm (no affine,
+    eps 1e-5) as the library reference; an image without text gets zeros."""
+    rng = np.random.default_rng(4)
+    dt, h = 48, 64
+    E = rng.standard_normal((5 + 0 + 3, dt))
+    off = np.array([0, 5, 5, 8])
+    Wt = rng.standard_normal((h, dt)) / math.sqrt(dt)
+    ctx = oracle.text_context(E, off, Wt, g_text=1.0, ln_eps=1e-5)
+    T = torch.from_numpy(E) @ torch.from_numpy(Wt).t()
+    LN = torch.nn.functional.layer_norm(T, (h,), eps=1e-5)
+    want0 = LN[0:5].mean(0).float().double().numpy()
+    want2 = LN[5:8].mean(0).float().double().numpy()
+    assert np.array_equal(ctx[0], want0) or np.abs(ctx[0] - want0).max() < 1e-6
+    assert np.abs(ctx[2] - want2).max() < 1e-6
+    assert not ctx[1].any()
+    ctx_half = oracle.text_context(E, off, Wt, g_text=0.5)
+    assert np.abs(ctx_half[0] - 0.5 * want0).max() < 1e-6
+
+
+# ---------------------------------------------------------------- selection vs a library attention
+
+def _random_episode(rng, n, h, scale=1.0):
+    K = rng.standard_normal((n, h)) * scale
+    Q = rng.standard_normal((n, h)) * scale
+    V = rng.standard_normal((n, h)) * scale
+    start = tuple(rng.standard_normal(h) for _ in range(3))
+    k_stop = rng.standard_normal(h)
+    c = rng.standard_normal(h) * 0.3
+    return K, Q, V, start, k_stop, c
+
+
+def _torch_step(K, Q, V, start, k_stop, c, hist, b, h):
+    """One pointer step recomputed with torch's scaled_dot_product_attention
+    for the causal history attention (the newest entry's query against all
+    history keys and values) and torch matmul for the pointer logits."""
+    k_s, q_s, v_s = start
+    Kx = np.vstack([K, k_s]); Qx = np.vstack([Q, q_s]); Vx = np.vstack([V, v_s])
+    rows = [K.shape[0] if x == "START" else x for x in hist]
+    e = rows[-1]
+    q = torch.from_numpy(Qx[e]).view(1, 1, 1, h)
+    kk = torch.from_numpy(Kx[rows]).view(1, 1, len(rows), h)
+    vv = torch.from_numpy(Vx[rows]).view(1, 1, len(rows), h)
+    att = torch.nn.functional.scaled_dot_product_attention(q, kk, vv, scale=1.0 / math.sqrt(h))
+    u = torch.from_numpy(c) + torch.from_numpy(Qx[e]) + att.view(h)
+    logits = (torch.from_numpy(K) @ u) / math.sqrt(h)
+    stop = float(torch.dot(torch.from_numpy(k_stop), u) / math.sqrt(h)) + b
+    return logits.numpy(), stop
+
+
+def test_every_history_of_a_tiny_episode_matches_library_attention():
+    """Brute force over every ordered history of length <= 3 on n = 5 tokens:
+    forced replays give, at every node, the logits that torch's attention and
+    matmul give, and the argmax follows the tie and STOP rules (Eq. 4)."""
+    rng = np.random.default_rng(11)
+    n, h, b = 5, 4, 0.1
+    K, Q, V, start, k_stop, c = _random_episode(rng, n, h)
+    for length in range(0, 4):
+        for seq in itertools.permutations(range(n), length):
+            res = oracle.run_episode(K, Q, V, start, k_stop, c, length + 1, b, h,
+                                     forced=list(seq) + [STOP])
+            assert len(res.steps) == length + 1
+            for t, step in enumerate(res.steps):
+                hist = ["START"] + list(seq[:t])
+                want, want_stop = _torch_step(K, Q, V, start, k_stop, c, hist, b, h)
+                want = want.copy()
+                want[list(seq[:t])] = -np.inf
+                fin = np.isfinite(want)
+                assert np.allclose(step.logits[fin], want[fin], rtol=0, atol=1e-12)
+                assert (step.logits[~fin] == -np.inf).all()
+                assert abs(step.stop_logit - want_stop) < 1e-12
+                cand = torch.from_numpy(np.append(want, want_stop))
+                assert step.argmax == (STOP if int(torch.argmax(cand)) == n else int(torch.argmax(cand))) \
+                    or cand[n] == cand.max()
+
+
+def test_greedy_trajectory_is_argmax_path():
+    """Free running, every action is the argmax of its own step and the run ends
+    at the first STOP or the cap (Eq. 2, Eq. 4, Algorithm 1 step 3)."""
+    rng = np.random.default_rng(12)
+    for trial in range(20):
+        n, h = int(rng.integers(2, 9)), int(rng.integers(1, 6))
+        K, Q, V, start, k_stop, c = _random_episode(rng, n, h)
+        cap = int(rng.integers(1, n + 3))
+        b = float(rng.normal())
+        res = oracle.run_episode(K, Q, V, start, k_stop, c, cap, b, h)
+        for t, step in enumerate(res.steps):
+            hist = ["START"] + res.actions[:t]
+            want, want_stop = _torch_step(K, Q, V, start, k_stop, c, hist, b, h)
+            want[res.actions[:t]] = -np.inf
+            if np.isfinite(want).any():
+                j = int(np.argmax(want))
+                exp = STOP if want_stop > want[j] else j
+            else:
+                exp = STOP
+            assert step.action == exp
+        assert len(res.actions) <= min(cap, n)
+        if not res.stopped:
+            assert len(res.actions) == min(cap, n) or len(res.actions) == cap
+
+
+# ---------------------------------------------------------------- P3 / P4: no-history reduction
+
+def test_no_history_is_topk_of_first_scores():
+    """Removing the history collapses the selector to Eq. 1's top-K of the first
+    step's scores: K = min(cap, #{l_1(j) > l_1(STOP)}), order descending with the
+    lowest index first on ties (torch.topk on a stably sorted copy)."""
+    rng = np.random.default_rng(13)
+    for trial in range(30):
+        n, h = int(rng.integers(1, 40)), int(rng.integers(1, 9))
+        K, Q, V, start, k_stop, c = _random_episode(rng, n, h)
+        if trial % 3 == 0:        # exact duplicates to exercise the tie rule
+            K[n // 2] = K[0]
+        cap = int(rng.integers(1, n + 2))
+        b = float(rng.normal())
+        res = oracle.run_episode(K, Q, V, start, k_stop, c, cap, b, h, no_history=True)
+        u1 = torch.from_numpy(c + start[1] + start[2])         # history [START]: softmax weight 1
+        l1 = (torch.from_numpy(K) @ u1) / math.sqrt(h)
+        stop1 = float(torch.dot(torch.from_numpy(k_stop), u1) / math.sqrt(h)) + b
+        order = torch.sort(l1, descending=True, stable=True).indices.tolist()
+        k = min(cap, int((l1 > stop1).sum()))
+        assert res.actions == order[:k]
+        assert res.stopped == (k < cap)
+
+
+def test_no_history_kept_set_maximises_score_sum_bruteforce():
+    """Brute force over all K-subsets on tiny n: the no-history kept set has the
+    largest sum of first-step logits among subsets of its size."""
+    rng = np.random.default_rng(14)
+    for trial in range(25):
+        n, h = int(rng.integers(2, 8)), int(rng.integers(1, 5))
+        K, Q, V, start, k_stop, c = _random_episode(rng, n, h)
+        cap = int(rng.integers(1, n + 1))
+        res = oracle.run_episode(K, Q, V, start, k_stop, c, cap, -0.5, h, no_history=True)
+        l1 = res.steps[0].logits
+        k = len(res.actions)
+        best = max(sum(l1[list(s)]) for s in itertools.combinations(range(n), k)) if k else 0.0
+        assert abs(sum(l1[res.actions]) - best) < 1e-12
+
+
+# ---------------------------------------------------------------- invariants on generated workloads
+
+def _pipeline(name, b=None, images=None):
+    w = W.WORKLOADS[name]
+    inp = W.make_inputs(w, images)
+    lay = W.make_layout(w, images)
+    KQV = oracle.project(inp["X"], inp["s_start"], inp["s_stop"], inp["W_kqv"], w.dtype)
+    ctx = oracle.text_context(inp["E_text"], lay.text_off, inp["W_text"])
+    if b is None:
+        b = W.stop_bias(w)
+    return w, inp, lay, KQV, ctx, b
+
+
+@pytest.fixture(scope="module")
+def tiny_bf16():
+    return _pipeline("tiny_bf16", b=1.0)
+
+
+def test_immediate_stop_gives_empty_selection(tiny_bf16):
+    """P1: STOP at the first step gives K = T* - 1 = 0 for every episode (Eq. 2)
+    and the prefill holds only the text rows."""
+    w, inp, lay, KQV, ctx, _ = tiny_bf16
+    res = oracle.select(KQV, ctx, lay.img_off, lay.grp_off, lay.grp_img, lay.grp_cap, math.inf, w.h)
+    assert all(e.actions == [] and e.stopped and e.n_steps == 1 for e in res.episodes)
+    pm = oracle.stop_thresholds(KQV, ctx, lay.grp_off, lay.grp_img, lay.grp_cap, w.h)
+    b_just = float(max(p[0] for p in pm)) + 1e-9
+    res2 = oracle.select(KQV, ctx, lay.img_off, lay.grp_off, lay.grp_img, lay.grp_cap, b_just, w.h)
+    assert not res2.kept_cnt.any()
+    out0 = np.full((lay.out_rows, w.d), -7.0)
+    out, seq = oracle.compact(inp["X"], lay.img_off, inp["E_text"], lay.text_off, res.kept,
+                              w.layout, lay.rows_per_image, out0)
+    for b_ in range(lay.batch):
+        L = lay.text_off[b_ + 1] - lay.text_off[b_]
+        base = b_ * lay.rows_per_image
+        assert np.array_equal(out[base:base + L], inp["E_text"][lay.text_off[b_]:lay.text_off[b_ + 1]])
+        assert seq[b_] == L
+
+
+@pytest.mark.parametrize("name", ["tiny_f32", "tiny_bf16", "small_packed_bf16"])
+def test_selection_invariants(name):
+    """P2: kept indices are unique, inside their group, at most the cap; an
+    episode takes K or K + 1 steps; the image list is ascending (Algorithm 1
+    step 4) and the concatenation of its groups."""
+    w, inp, lay, KQV, ctx, b = _pipeline(name)
+    res = oracle.select(KQV, ctx, lay.img_off, lay.grp_off, lay.grp_img, lay.grp_cap, b, w.h)
+    for g, ep in enumerate(res.episodes):
+        n = lay.grp_off[g + 1] - lay.grp_off[g]
+        assert len(set(ep.actions)) == len(ep.actions)
+        assert all(0 <= a < n for a in ep.actions)
+        assert len(ep.actions) <= lay.grp_cap[g]
+        assert ep.n_steps in (len(ep.actions), len(ep.actions) + 1)
+        assert ep.stopped or len(ep.actions) == min(lay.grp_cap[g], n)
+    for b_ in range(lay.batch):
+        k = res.kept[b_]
+        assert k == sorted(k) and len(set(k)) == len(k)
+        assert len(k) <= lay.kept_off[b_ + 1] - lay.kept_off[b_]
+    assert res.kept_cnt.sum() == res.grp_cnt.sum()
+
+
+def test_stop_bias_prefix_property(tiny_bf16):
+    """P5: the bias only enters the STOP logit, so for b1 < b2 the trajectory at
+    b2 is a prefix of the trajectory at b1, and K(b) = #{t: min(m_1..m_t) >= b}."""
+    w, inp, lay, KQV, ctx, _ = tiny_bf16
+    pm = oracle.stop_thresholds(KQV, ctx, lay.grp_off, lay.grp_img, lay.grp_cap, w.h)
+    prev = None
+    for b in (-3.0, 0.2, 0.9, 1.3, 2.5):
+        res = oracle.select(KQV, ctx, lay.img_off, lay.grp_off, lay.grp_img, lay.grp_cap, b, w.h)
+        for g, ep in enumerate(res.episodes):
+            assert len(ep.actions) == int(np.count_nonzero(pm[g] >= b))
+            if prev is not None:
+                assert prev.episodes[g].actions[:len(ep.actions)] == ep.actions
+        prev = res
+
+
+def test_cap_prefix_property(tiny_bf16):
+    """P6: the trajectory under cap C is the first C actions under a larger cap."""
+    w, inp, lay, KQV, ctx, b = tiny_bf16
+    caps = lay.grp_cap.copy()
+    full = oracle.select(KQV, ctx, lay.img_off, lay.grp_off, lay.grp_img, caps * 3, -math.inf, w.h)
+    for c in (1, 3, 7):
+        res = oracle.select(KQV, ctx, lay.img_off, lay.grp_off, lay.grp_img, np.full_like(caps, c), -math.inf, w.h)
+        for g, ep in enumerate(res.episodes):
+            assert ep.actions == full.episodes[g].actions[:c]
+
+
+def test_episode_independence():
+    """P7: an image's result does not depend on the other images of the batch or
+    their order (each group is its own episode)."""
+    name = "tiny_bf16"
+    w, inp, lay, KQV, ctx, _ = _pipeline(name, b=1.0)
+    full = oracle.select(KQV, ctx, lay.img_off, lay.grp_off, lay.grp_img, lay.grp_cap, 1.0, w.h)
+    sub = [3, 0]
+    w2, inp2, lay2, KQV2, ctx2, _ = _pipeline(name, b=1.0, images=sub)
+    part = oracle.select(KQV2, ctx2, lay2.img_off, lay2.grp_off, lay2.grp_img, lay2.grp_cap, 1.0, w.h)
+    for i, b_ in enumerate(sub):
+        assert part.kept[i] == full.kept[b_]
+
+
+def test_permutation_equivariance():
+    """P8: the selector takes no positional input, so permuting a group's rows
+    permutes the selected tokens the same way (no exact ties here)."""
+    rng = np.random.default_rng(15)
+    n, h = 30, 8
+    K, Q, V, start, k_stop, c = _random_episode(rng, n, h)
+    res = oracle.run_episode(K, Q, V, start, k_stop, c, 12, 0.3, h)
+    perm = rng.permutation(n)
+    inv = np.argsort(perm)
+    res_p = oracle.run_episode(K[perm], Q[perm], V[perm], start, k_stop, c, 12, 0.3, h)
+    assert [int(perm[a]) for a in res_p.actions] == res.actions
+    assert [int(inv[a]) for a in res.actions] == res_p.actions
+
+
+def test_never_stop_keeps_everything_and_compaction_is_identity(tiny_bf16):
+    """P9: with b = -inf and a cap >= n every token is kept (only STOP remains at
+    step n + 1) and the compacted sequence is [X_b; E_b] bit for bit
+    (Algorithm 1 steps 4-5)."""
+    w, inp, lay, KQV, ctx, _ = tiny_bf16
+    sizes = np.diff(lay.grp_off)
+    caps = sizes + 2
+    res = oracle.select(KQV, ctx, lay.img_off, lay.grp_off, lay.grp_img, caps, -math.inf, w.h)
+    for g, ep in enumerate(res.episodes):
+        assert sorted(ep.actions) == list(range(sizes[g])) and ep.stopped
+        assert ep.n_steps == sizes[g] + 1
+    out0 = np.zeros((lay.out_rows, w.d))
+    out, seq = oracle.compact(inp["X"], lay.img_off, inp["E_text"], lay.text_off, res.kept,
+                              "padded", lay.rows_per_image, out0)
+    for b_ in range(lay.batch):
+        want = np.vstack([inp["X"][lay.img_off[b_]:lay.img_off[b_ + 1]],
+                          inp["E_text"][lay.text_off[b_]:lay.text_off[b_ + 1]]])
+        base = b_ * lay.rows_per_image
+        assert np.array_equal(out[base:base + len(want)], want)
+        assert seq[b_] == len(want)
+
+
+def test_duplicate_rows_lower_index_first():
+    """P10: two tokens with identical rows get identical logits; the lower index
+    is taken first (first maximal index)."""
+    rng = np.random.default_rng(16)
+    n, h = 12, 6
+    K, Q, V, start, k_stop, c = _random_episode(rng, n, h)
+    u1 = c + start[1] + start[2]
+    top = int(np.argmax(K @ u1))
+    dup = (top + 5) % n
+    K[dup], Q[dup], V[dup] = K[top], Q[top], V[top]
+    lo, hi = min(top, dup), max(top, dup)
+    res = oracle.run_episode(K, Q, V, start, k_stop, c, 3, -math.inf, h)
+    assert res.steps[0].logits[lo] == res.steps[0].logits[hi]
+    assert res.actions[0] == lo
+
+
+def test_packed_compaction_against_library_scan():
+    """Packed layout: cu_seqlens is the exclusive prefix sum of K_b + L_b (torch
+    cumsum as reference), rows are X rows in ascending order then text rows,
+    and rows beyond cu[B] are untouched."""
+    w, inp, lay, KQV, ctx, b = _pipeline("small_packed_bf16")
+    res = oracle.select(KQV, ctx, lay.img_off, lay.grp_off, lay.grp_img, lay.grp_cap, b, w.h)
+    out0 = np.full((lay.out_rows, w.d), 123.0)
+    out, cu = oracle.compact(inp["X"], lay.img_off, inp["E_text"], lay.text_off, res.kept,
+                             "packed", 0, out0)
+    lens = torch.tensor([len(k) + int(lay.text_off[i + 1] - lay.text_off[i]) for i, k in enumerate(res.kept)])
+    assert cu.tolist() == [0] + torch.cumsum(lens, 0).tolist()
+    for b_ in range(lay.batch):
+        k = res.kept[b_]
+        rows = out[cu[b_]:cu[b_] + len(k)]
+        for r, idx in zip(rows, k):
+            assert np.array_equal(r, inp["X"][lay.img_off[b_] + idx])
+    assert (out[cu[-1]:] == 123.0).all()
+
+
+def test_calibrated_bias_reproduces_predicted_counts():
+    """The stored bias of a small workload, re-run from scratch, retains exactly
+    the count its calibration predicted (STOP bias self-check)."""
+    import json as _json
+    with open(W.STOP_BIAS_FILE) as f:
+        table = _json.load(f)
+    for name in ("tiny_f32", "tiny_bf16", "small_packed_bf16"):
+        w, inp, lay, KQV, ctx, b = _pipeline(name)
+        res = oracle.select(KQV, ctx, lay.img_off, lay.grp_off, lay.grp_img, lay.grp_cap, b, w.h)
+        assert int(res.kept_cnt.sum()) == table[name]["retained_total"]
