@@ -1,0 +1,141 @@
+"""Thin ctypes binding of libstepprune (include/stepprune.h).
+
+Argument marshalling only: torch tensors are passed by ``data_ptr()``, the
+stream is torch's current HIP stream unless given, and a status other than
+SP_OK raises ``StepPruneError``.  Every computation runs in the library's HIP
+kernels.  Importing this module fails loudly if the library has not been
+built (``python -m paper_2609_13804_amd.build``).
+"""
+import ctypes
+import os
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libstepprune.so")
+
+SP_OK, SP_EINVAL, SP_EUNSUPPORTED, SP_EWORKSPACE, SP_EHIP, SP_EDEVICE = range(6)
+SP_F32, SP_BF16 = 0, 1
+SP_TRACE, SP_NO_HISTORY = 1, 2
+SP_LAYOUT_PADDED, SP_LAYOUT_PACKED = 0, 1
+SP_DEV_OK, SP_DEV_BAD_OFFSETS, SP_DEV_GROUP_TOO_LARGE, SP_DEV_BAD_CAP, SP_DEV_OUTPUT_OVERFLOW = range(5)
+STAGE_PROJECT, STAGE_SELECT, STAGE_COMPACT = 0, 1, 2
+
+EXPORTS = ["stepprune_project", "stepprune_select", "stepprune_compact",
+           "stepprune_workspace_bytes", "stepprune_read_device_error", "stepprune_status_string"]
+
+
+class StepPruneError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn}: {status_string(status)} (status {status})")
+
+
+class sp_dims(ctypes.Structure):
+    _fields_ = [("d", ctypes.c_int32), ("d_text", ctypes.c_int32),
+                ("h", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_13804_amd.build`")
+_lib = ctypes.CDLL(LIB_PATH)
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+_F32 = ctypes.c_float
+_SZ = ctypes.c_size_t
+_DIMS = ctypes.POINTER(sp_dims)
+
+_lib.stepprune_project.restype = _I32
+_lib.stepprune_project.argtypes = [_DIMS, _P, _I64, _P, _P, _P, _P, _P, _I32, _I64, _P, _F32, _F32,
+                                   _P, _P, _P, _SZ, _P]
+_lib.stepprune_select.restype = _I32
+_lib.stepprune_select.argtypes = [_DIMS, _P, _P, _I64, _P, _I32, _P, _P, _P, _I32, _I32, _I32, _P,
+                                  _F32, _I32, ctypes.c_uint32, _P, _P, _P, _P, _I32, _P, _SZ, _P]
+_lib.stepprune_compact.restype = _I32
+_lib.stepprune_compact.argtypes = [_DIMS, _P, _P, _P, _P, _P, _P, _P, _I32, _I32, _I32, _I64, _P, _P,
+                                   _P, _SZ, _P]
+_lib.stepprune_workspace_bytes.restype = _SZ
+_lib.stepprune_workspace_bytes.argtypes = [_I32, _DIMS, _I64, _I64, _I32, _I32, _I32, _I32]
+_lib.stepprune_read_device_error.restype = _I32
+_lib.stepprune_read_device_error.argtypes = [_P, _P, ctypes.POINTER(_I32)]
+_lib.stepprune_status_string.restype = ctypes.c_char_p
+_lib.stepprune_status_string.argtypes = [_I32]
+
+
+def library():
+    return _lib
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def dims(d: int, d_text: int, h: int, dtype: int) -> sp_dims:
+    return sp_dims(d, d_text, h, dtype)
+
+
+def status_string(status: int) -> str:
+    return _lib.stepprune_status_string(status).decode()
+
+
+def _check(fn, status, raise_on_error):
+    if raise_on_error and status != SP_OK:
+        raise StepPruneError(fn, status)
+    return status
+
+
+def stepprune_workspace_bytes(which, dm, T_vis, T_txt, B, G, max_group, max_cap) -> int:
+    return int(_lib.stepprune_workspace_bytes(which, ctypes.byref(dm), T_vis, T_txt, B, G,
+                                              max_group, max_cap))
+
+
+def stepprune_project(dm, X, T_vis, s_start, s_stop, W_kqv, E_text, text_off, B, T_txt, W_text,
+                      g_text, ln_eps, KQV, ctx, ws, ws_bytes, stream=None, raise_on_error=True):
+    st = _lib.stepprune_project(ctypes.byref(dm), _ptr(X), T_vis, _ptr(s_start), _ptr(s_stop),
+                                _ptr(W_kqv), _ptr(E_text), _ptr(text_off), B, T_txt, _ptr(W_text),
+                                g_text, ln_eps, _ptr(KQV), _ptr(ctx), _ptr(ws), ws_bytes,
+                                _stream(stream))
+    return _check("stepprune_project", st, raise_on_error)
+
+
+def stepprune_select(dm, KQV, ctx, T_vis, img_off, B, grp_off, grp_img, grp_cap, G, max_group,
+                     max_cap, kept_off, b_stop, g, flags, kept_idx, kept_cnt, grp_cnt, trace,
+                     trace_steps, ws, ws_bytes, stream=None, raise_on_error=True):
+    st = _lib.stepprune_select(ctypes.byref(dm), _ptr(KQV), _ptr(ctx), T_vis, _ptr(img_off), B,
+                               _ptr(grp_off), _ptr(grp_img), _ptr(grp_cap), G, max_group, max_cap,
+                               _ptr(kept_off), b_stop, g, flags, _ptr(kept_idx), _ptr(kept_cnt),
+                               _ptr(grp_cnt), _ptr(trace), trace_steps, _ptr(ws), ws_bytes,
+                               _stream(stream))
+    return _check("stepprune_select", st, raise_on_error)
+
+
+def stepprune_compact(dm, X, img_off, E_text, text_off, kept_idx, kept_off, kept_cnt, B, layout,
+                      rows_per_image, out_rows, out, seq_info, ws, ws_bytes, stream=None,
+                      raise_on_error=True):
+    st = _lib.stepprune_compact(ctypes.byref(dm), _ptr(X), _ptr(img_off), _ptr(E_text),
+                                _ptr(text_off), _ptr(kept_idx), _ptr(kept_off), _ptr(kept_cnt), B,
+                                layout, rows_per_image, out_rows, _ptr(out), _ptr(seq_info),
+                                _ptr(ws), ws_bytes, _stream(stream))
+    return _check("stepprune_compact", st, raise_on_error)
+
+
+def stepprune_read_device_error(ws, stream=None) -> int:
+    code = _I32(0)
+    st = _lib.stepprune_read_device_error(_ptr(ws), _stream(stream), ctypes.byref(code))
+    if st not in (SP_OK, SP_EDEVICE):
+        raise StepPruneError("stepprune_read_device_error", st)
+    return int(code.value)

@@ -1,0 +1,226 @@
+// C ABI of libstepprune (include/stepprune.h): host-side validation, workspace
+// layout and launch order.  Every entry point validates its arguments before
+// touching the device and never throws.
+#include <string.h>
+
+#include "sp_internal.h"
+
+using namespace sp;
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+sp_status check_dims(const sp_dims* d) {
+  if (!d) return SP_EINVAL;
+  if (d->d <= 0 || d->d_text <= 0 || d->h <= 0) return SP_EINVAL;
+  if (d->d % 64 || d->d_text % 64 || d->h % 64) return SP_EINVAL;
+  if (d->dtype != SP_F32 && d->dtype != SP_BF16) return SP_EUNSUPPORTED;
+  if (d->h > 1024) return SP_EUNSUPPORTED;
+  return SP_OK;
+}
+
+int elem_bytes(const sp_dims* d) { return d->dtype == SP_F32 ? 4 : 2; }
+
+struct SelectWs {
+  size_t gram, ck, kept, count, total;
+  int64_t gstride;
+  int gram_ld, ck_ld;
+};
+
+SelectWs select_ws_layout(int G, int max_group, int max_cap) {
+  SelectWs w;
+  w.gram_ld = (int)align_up((size_t)max_group + 2, 4);
+  w.ck_ld = (int)align_up((size_t)max_group + 1, 4);
+  w.gstride = (int64_t)2 * (max_group + 1) * w.gram_ld;
+  size_t off = kWsHeaderBytes;
+  w.gram = off;
+  off = align_up(off + (size_t)G * w.gstride * 4, 256);
+  w.ck = off;
+  off = align_up(off + (size_t)G * w.ck_ld * 4, 256);
+  w.kept = off;
+  off = align_up(off + (size_t)G * (max_cap > 0 ? max_cap : 1) * 4, 256);
+  w.count = off;
+  off = align_up(off + (size_t)G * 4, 256);
+  w.total = off;
+  return w;
+}
+
+size_t project_ws_bytes(const sp_dims* d, int64_t T_txt) {
+  return kWsHeaderBytes + align_up((size_t)T_txt * d->h * 4, 256);
+}
+
+sp_status hip_status(hipError_t e) { return e == hipSuccess ? SP_OK : SP_EHIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* stepprune_status_string(sp_status s) {
+  switch (s) {
+    case SP_OK: return "ok";
+    case SP_EINVAL: return "invalid argument";
+    case SP_EUNSUPPORTED: return "unsupported argument";
+    case SP_EWORKSPACE: return "workspace too small";
+    case SP_EHIP: return "HIP runtime error";
+    case SP_EDEVICE: return "device-side error (see stepprune_read_device_error)";
+  }
+  return "unknown status";
+}
+
+size_t stepprune_workspace_bytes(int32_t which, const sp_dims* dims, int64_t T_vis, int64_t T_txt,
+                                 int32_t B, int32_t G, int32_t max_group, int32_t max_cap) {
+  if (check_dims(dims) != SP_OK || T_vis < 0 || T_txt < 0 || B < 0 || G < 0) return 0;
+  switch (which) {
+    case 0: return project_ws_bytes(dims, T_txt);
+    case 1:
+      if (max_group < 0 || max_group > kMaxGroup || max_cap < 0) return 0;
+      return select_ws_layout(G, max_group, max_cap).total;
+    case 2: return kWsHeaderBytes;
+  }
+  return 0;
+}
+
+sp_status stepprune_project(const sp_dims* dims, const void* X, int64_t T_vis, const void* s_start,
+                            const void* s_stop, const void* W_kqv, const void* E_text,
+                            const int32_t* text_off, int32_t B, int64_t T_txt, const void* W_text,
+                            float g_text, float ln_eps, void* KQV, float* ctx, void* ws,
+                            size_t ws_bytes, hipStream_t stream) {
+  sp_status st = check_dims(dims);
+  if (st != SP_OK) return st;
+  if (T_vis < 0 || T_txt < 0 || B < 1) return SP_EINVAL;
+  if (!s_start || !s_stop || !W_kqv || !KQV || !ctx || !text_off || !W_text || !ws) return SP_EINVAL;
+  if ((T_vis > 0 && !X) || (T_txt > 0 && !E_text)) return SP_EINVAL;
+  if (!aligned16(X) || !aligned16(s_start) || !aligned16(s_stop) || !aligned16(W_kqv) ||
+      !aligned16(E_text) || !aligned16(W_text) || !aligned16(KQV) || !aligned16(ctx) ||
+      !aligned16(ws))
+    return SP_EINVAL;
+  if (!(ln_eps >= 0.0f)) return SP_EINVAL;
+  if (ws_bytes < project_ws_bytes(dims, T_txt)) return SP_EWORKSPACE;
+
+  int32_t* err = reinterpret_cast<int32_t*>(ws);
+  float* tproj = reinterpret_cast<float*>(static_cast<char*>(ws) + kWsHeaderBytes);
+  hipError_t e = launch_clear_error(err, stream);
+  if (e == hipSuccess)
+    e = launch_project_gemm(dims->dtype, X, T_vis, s_start, s_stop, W_kqv, dims->d, 3 * dims->h,
+                            KQV, stream);
+  if (e == hipSuccess)
+    e = launch_text_gemm(dims->dtype, E_text, T_txt, W_text, dims->d_text, dims->h, tproj, stream);
+  if (e == hipSuccess)
+    e = launch_text_pool(tproj, text_off, B, T_txt, dims->h, g_text, ln_eps, ctx, err, stream);
+  return hip_status(e);
+}
+
+sp_status stepprune_select(const sp_dims* dims, const void* KQV, const float* ctx, int64_t T_vis,
+                           const int32_t* img_off, int32_t B, const int32_t* grp_off,
+                           const int32_t* grp_img, const int32_t* grp_cap, int32_t G,
+                           int32_t max_group, int32_t max_cap, const int32_t* kept_off,
+                           float b_stop, int32_t g, uint32_t flags, int32_t* kept_idx,
+                           int32_t* kept_cnt, int32_t* grp_cnt, float* trace, int32_t trace_steps,
+                           void* ws, size_t ws_bytes, hipStream_t stream) {
+  sp_status st = check_dims(dims);
+  if (st != SP_OK) return st;
+  if (T_vis < 0 || B < 1 || G < 0 || max_group < 0 || max_cap < 0 || trace_steps < 0)
+    return SP_EINVAL;
+  if (g < 1) return SP_EINVAL;
+  if (g > 1) return SP_EUNSUPPORTED;
+  if (max_group > kMaxGroup) return SP_EUNSUPPORTED;
+  if (flags & ~(uint32_t)(SP_TRACE | SP_NO_HISTORY)) return SP_EINVAL;
+  if (!KQV || !ctx || !img_off || !kept_off || !kept_cnt || !ws) return SP_EINVAL;
+  if (G > 0 && (!grp_off || !grp_img || !grp_cap || !kept_idx)) return SP_EINVAL;
+  if ((flags & SP_TRACE) && trace_steps > 0 && !trace) return SP_EINVAL;
+  if (b_stop != b_stop) return SP_EINVAL;   // NaN
+  if (!aligned16(KQV) || !aligned16(ctx) || !aligned16(ws)) return SP_EINVAL;
+  const SelectWs lay = select_ws_layout(G, max_group, max_cap);
+  if (ws_bytes < lay.total) return SP_EWORKSPACE;
+
+  char* wsb = static_cast<char*>(ws);
+  SelectArgs a;
+  a.dtype = dims->dtype;
+  a.KQV = KQV;
+  a.ctx = ctx;
+  a.T_vis = T_vis;
+  a.h = dims->h;
+  a.img_off = img_off;
+  a.B = B;
+  a.grp_off = grp_off;
+  a.grp_img = grp_img;
+  a.grp_cap = grp_cap;
+  a.G = G;
+  a.max_group = max_group;
+  a.max_cap = max_cap > 0 ? max_cap : 1;
+  a.kept_off = kept_off;
+  a.b_stop = b_stop;
+  a.flags = flags;
+  a.kept_idx = kept_idx;
+  a.kept_cnt = kept_cnt;
+  a.grp_cnt = grp_cnt;
+  a.trace = trace;
+  a.trace_steps = trace_steps;
+  a.gram = reinterpret_cast<float*>(wsb + lay.gram);
+  a.gram_group_stride = lay.gstride;
+  a.gram_ld = lay.gram_ld;
+  a.cK = reinterpret_cast<float*>(wsb + lay.ck);
+  a.ck_ld = lay.ck_ld;
+  a.grp_kept = reinterpret_cast<int32_t*>(wsb + lay.kept);
+  a.grp_count = reinterpret_cast<int32_t*>(wsb + lay.count);
+  a.err = reinterpret_cast<int32_t*>(wsb);
+  hipError_t e = launch_clear_error(a.err, stream);
+  if (e == hipSuccess) e = launch_select(a, stream);
+  return hip_status(e);
+}
+
+sp_status stepprune_compact(const sp_dims* dims, const void* X, const int32_t* img_off,
+                            const void* E_text, const int32_t* text_off, const int32_t* kept_idx,
+                            const int32_t* kept_off, const int32_t* kept_cnt, int32_t B,
+                            int32_t layout, int32_t rows_per_image, int64_t out_rows, void* out,
+                            int32_t* seq_info, void* ws, size_t ws_bytes, hipStream_t stream) {
+  sp_status st = check_dims(dims);
+  if (st != SP_OK) return st;
+  if (dims->d_text != dims->d) return SP_EUNSUPPORTED;
+  if (B < 1 || out_rows < 0) return SP_EINVAL;
+  if (layout != SP_LAYOUT_PADDED && layout != SP_LAYOUT_PACKED) return SP_EINVAL;
+  if (layout == SP_LAYOUT_PADDED && (rows_per_image < 0 || (int64_t)rows_per_image * B > out_rows))
+    return SP_EINVAL;
+  if (!X || !img_off || !E_text || !text_off || !kept_idx || !kept_off || !kept_cnt || !out ||
+      !seq_info || !ws)
+    return SP_EINVAL;
+  if (!aligned16(X) || !aligned16(E_text) || !aligned16(out) || !aligned16(ws)) return SP_EINVAL;
+  if (ws_bytes < kWsHeaderBytes) return SP_EWORKSPACE;
+  CompactArgs a;
+  a.elem_bytes = elem_bytes(dims);
+  a.d = dims->d;
+  a.X = X;
+  a.img_off = img_off;
+  a.E = E_text;
+  a.text_off = text_off;
+  a.kept_idx = kept_idx;
+  a.kept_off = kept_off;
+  a.kept_cnt = kept_cnt;
+  a.B = B;
+  a.layout = layout;
+  a.rows_per_image = rows_per_image;
+  a.out_rows = out_rows;
+  a.out = out;
+  a.seq_info = seq_info;
+  a.err = reinterpret_cast<int32_t*>(ws);
+  hipError_t e = launch_clear_error(a.err, stream);
+  if (e == hipSuccess) e = launch_compact(a, stream);
+  return hip_status(e);
+}
+
+sp_status stepprune_read_device_error(void* ws, hipStream_t stream, int32_t* code) {
+  if (!ws || !code) return SP_EINVAL;
+  if (hipStreamSynchronize(stream) != hipSuccess) return SP_EHIP;
+  int32_t v = 0;
+  if (hipMemcpy(&v, ws, sizeof(v), hipMemcpyDeviceToHost) != hipSuccess) return SP_EHIP;
+  *code = v;
+  if (v != 0) {
+    const int32_t zero = 0;
+    if (hipMemcpy(ws, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess) return SP_EHIP;
+    return SP_EDEVICE;
+  }
+  return SP_OK;
+}
+
+}  // extern "C"

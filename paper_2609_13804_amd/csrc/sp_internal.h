@@ -1,0 +1,106 @@
+// Internal declarations shared by the HIP translation units of libstepprune.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_bf16.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "stepprune.h"
+
+namespace sp {
+
+// Workspace header: the first 256 bytes of every workspace.
+struct WsHeader {
+  int32_t error;       // SP_DEV_* code, first error wins (atomicCAS from 0)
+  int32_t pad[63];
+};
+constexpr size_t kWsHeaderBytes = 256;
+
+constexpr int kMaxGroup = 1022;        // largest group the selection kernel takes
+constexpr int kLdsBytes = 160 * 1024;  // LDS per workgroup on gfx950
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+__device__ inline void set_device_error(int32_t* err, int32_t code) {
+  atomicCAS(err, 0, code);
+}
+
+// ---------------------------------------------------------------- GEMM launchers
+// C[m, n] = sum_k A[m, k] * B[n, k]  (both operands K-contiguous), fp32 accumulate.
+
+// Projection: A rows are X rows 0..T_vis-1, then s_start, then s_stop.
+hipError_t launch_project_gemm(int dtype, const void* X, int64_t T_vis, const void* s_start,
+                               const void* s_stop, const void* W, int d, int n_out, void* out,
+                               hipStream_t stream);
+// Text projection: A = E_text [T_txt, d_text], B = W_text [h, d_text], fp32 output.
+hipError_t launch_text_gemm(int dtype, const void* E, int64_t T_txt, const void* W, int d_text,
+                            int h, float* out, hipStream_t stream);
+// Per-group Gram products of the projected rows (see select.hip for the layout).
+hipError_t launch_gram_gemm(int dtype, const void* KQV, int64_t T_vis, int h,
+                            const int32_t* grp_off, int G, int max_group, float* gram,
+                            int64_t gram_group_stride, int gram_ld, int32_t* err,
+                            hipStream_t stream);
+
+// ---------------------------------------------------------------- other launchers
+hipError_t launch_text_pool(const float* T, const int32_t* text_off, int B, int64_t T_txt, int h,
+                            float g_text, float ln_eps, float* ctx, int32_t* err,
+                            hipStream_t stream);
+
+struct SelectArgs {
+  int dtype;
+  const void* KQV;
+  const float* ctx;
+  int64_t T_vis;
+  int h;
+  const int32_t* img_off;
+  int B;
+  const int32_t* grp_off;
+  const int32_t* grp_img;
+  const int32_t* grp_cap;
+  int G;
+  int max_group;
+  int max_cap;
+  const int32_t* kept_off;
+  float b_stop;
+  uint32_t flags;
+  int32_t* kept_idx;
+  int32_t* kept_cnt;
+  int32_t* grp_cnt;
+  float* trace;
+  int trace_steps;
+  // workspace pieces
+  float* gram;
+  int64_t gram_group_stride;
+  int gram_ld;
+  float* cK;             // [G, ck_ld]
+  int ck_ld;
+  int32_t* grp_kept;     // [G, max_cap]
+  int32_t* grp_count;    // [G]
+  int32_t* err;
+};
+hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
+
+struct CompactArgs {
+  int elem_bytes;
+  int d;
+  const void* X;
+  const int32_t* img_off;
+  const void* E;
+  const int32_t* text_off;
+  const int32_t* kept_idx;
+  const int32_t* kept_off;
+  const int32_t* kept_cnt;
+  int B;
+  int layout;
+  int rows_per_image;
+  int64_t out_rows;
+  void* out;
+  int32_t* seq_info;
+  int32_t* err;
+};
+hipError_t launch_compact(const CompactArgs& a, hipStream_t stream);
+
+hipError_t launch_clear_error(int32_t* err, hipStream_t stream);
+
+}  // namespace sp

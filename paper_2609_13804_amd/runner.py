@@ -1,0 +1,155 @@
+"""Device buffers for one batch and the three library calls in order.
+
+Plumbing only: torch allocates HBM and provides the stream; every stage runs
+in libstepprune's kernels through the binding.
+"""
+from dataclasses import dataclass
+from typing import Dict, Optional
+
+import numpy as np
+import torch
+
+from . import binding as sp
+from . import workloads as W
+
+
+def torch_dtype(dtype: str):
+    return torch.float32 if dtype == "f32" else torch.bfloat16
+
+
+@dataclass
+class Sizes:
+    T_vis: int
+    T_txt: int
+    B: int
+    G: int
+    max_group: int
+    max_cap: int
+    kept_total: int
+
+
+class DeviceRun:
+    """All inputs, outputs and workspaces of one batch, resident on the GPU."""
+
+    def __init__(self, w: W.Workload, inputs: Dict[str, np.ndarray], layout: W.Layout,
+                 b_stop: float, device="cuda", trace_steps: int = 0, flags: int = 0,
+                 caps: Optional[np.ndarray] = None, max_group: Optional[int] = None):
+        self.w = w
+        self.layout = layout
+        self.b_stop = float(b_stop)
+        self.flags = flags | (sp.SP_TRACE if trace_steps > 0 else 0)
+        self.trace_steps = trace_steps
+        dev = torch.device(device)
+        tdt = torch_dtype(w.dtype)
+        up = lambda a, dt=tdt: torch.from_numpy(np.ascontiguousarray(a)).to(device=dev, dtype=dt)
+        upi = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+        self.X = up(inputs["X"])
+        self.E = up(inputs["E_text"])
+        self.W_kqv = up(inputs["W_kqv"])
+        self.W_text = up(inputs["W_text"])
+        self.s_start = up(inputs["s_start"])
+        self.s_stop = up(inputs["s_stop"])
+        caps = layout.grp_cap if caps is None else np.asarray(caps, np.int32)
+        sizes = np.diff(layout.grp_off)
+        self.caps_host = caps
+        kept_per_img = np.zeros(layout.batch + 1, np.int64)
+        for g in range(layout.groups):
+            kept_per_img[layout.grp_img[g] + 1] += min(int(caps[g]), int(sizes[g]))
+        kept_off = np.cumsum(kept_per_img).astype(np.int32)
+        self.img_off = upi(layout.img_off)
+        self.text_off = upi(layout.text_off)
+        self.grp_off = upi(layout.grp_off)
+        self.grp_img = upi(layout.grp_img)
+        self.grp_cap = upi(caps)
+        self.kept_off = upi(kept_off)
+        self.kept_off_host = kept_off
+        self.sizes = Sizes(T_vis=int(layout.img_off[-1]), T_txt=int(layout.text_off[-1]),
+                           B=layout.batch, G=layout.groups,
+                           max_group=int(max_group if max_group is not None else
+                                         (sizes.max() if sizes.size else 0)),
+                           max_cap=int(max(1, max((min(int(c), int(n)) for c, n in zip(caps, sizes)),
+                                                  default=1))),
+                           kept_total=int(kept_off[-1]))
+        s = self.sizes
+        self.dims = sp.dims(w.d, w.d_text, w.h, sp.SP_F32 if w.dtype == "f32" else sp.SP_BF16)
+        self.KQV = torch.empty((s.T_vis + 2, 3 * w.h), dtype=tdt, device=dev)
+        self.ctx = torch.empty((s.B, w.h), dtype=torch.float32, device=dev)
+        self.kept_idx = torch.full((max(1, s.kept_total),), -1, dtype=torch.int32, device=dev)
+        self.kept_cnt = torch.zeros(s.B, dtype=torch.int32, device=dev)
+        self.grp_cnt = torch.zeros(max(1, s.G), dtype=torch.int32, device=dev)
+        self.trace = (torch.empty((s.G, trace_steps, 4), dtype=torch.float32, device=dev)
+                      if trace_steps > 0 else None)
+        if w.layout == "padded":
+            self.layout_code = sp.SP_LAYOUT_PADDED
+            self.rows_per_image = layout.rows_per_image
+            self.out_rows = s.B * layout.rows_per_image
+            self.seq_info = torch.zeros(s.B, dtype=torch.int32, device=dev)
+        else:
+            self.layout_code = sp.SP_LAYOUT_PACKED
+            self.rows_per_image = 0
+            self.out_rows = s.kept_total + s.T_txt
+            self.seq_info = torch.zeros(s.B + 1, dtype=torch.int32, device=dev)
+        self.out = (torch.zeros((self.out_rows, w.d), dtype=tdt, device=dev)
+                    if w.d_text == w.d else None)
+        nb = lambda which: sp.stepprune_workspace_bytes(which, self.dims, s.T_vis, s.T_txt, s.B,
+                                                        s.G, s.max_group, s.max_cap)
+        self.ws_bytes = [nb(sp.STAGE_PROJECT), nb(sp.STAGE_SELECT), nb(sp.STAGE_COMPACT)]
+        if min(self.ws_bytes) == 0:
+            raise ValueError("workspace size query rejected the sizes")
+        self.ws = [torch.zeros(n, dtype=torch.uint8, device=dev) for n in self.ws_bytes]
+
+    # ---------------------------------------------------------------- stages
+    def project(self, stream=None, g_text: float = 1.0, ln_eps: float = 1e-5):
+        s = self.sizes
+        return sp.stepprune_project(self.dims, self.X, s.T_vis, self.s_start, self.s_stop,
+                                    self.W_kqv, self.E, self.text_off, s.B, s.T_txt, self.W_text,
+                                    g_text, ln_eps, self.KQV, self.ctx, self.ws[0],
+                                    self.ws_bytes[0], stream)
+
+    def select(self, stream=None, b_stop: Optional[float] = None, flags: Optional[int] = None):
+        s = self.sizes
+        return sp.stepprune_select(self.dims, self.KQV, self.ctx, s.T_vis, self.img_off, s.B,
+                                   self.grp_off, self.grp_img, self.grp_cap, s.G, s.max_group,
+                                   s.max_cap, self.kept_off,
+                                   self.b_stop if b_stop is None else b_stop, 1,
+                                   self.flags if flags is None else flags, self.kept_idx,
+                                   self.kept_cnt, self.grp_cnt, self.trace, self.trace_steps,
+                                   self.ws[1], self.ws_bytes[1], stream)
+
+    def compact(self, stream=None):
+        s = self.sizes
+        return sp.stepprune_compact(self.dims, self.X, self.img_off, self.E, self.text_off,
+                                    self.kept_idx, self.kept_off, self.kept_cnt, s.B,
+                                    self.layout_code, self.rows_per_image, self.out_rows, self.out,
+                                    self.seq_info, self.ws[2], self.ws_bytes[2], stream)
+
+    def run(self, stream=None):
+        self.project(stream)
+        self.select(stream)
+        if self.out is not None:
+            self.compact(stream)
+
+    def device_errors(self):
+        return [sp.stepprune_read_device_error(ws) for ws in self.ws]
+
+    # ---------------------------------------------------------------- results
+    def kept_lists(self):
+        cnt = self.kept_cnt.cpu().numpy()
+        idx = self.kept_idx.cpu().numpy()
+        off = self.kept_off_host
+        return [idx[off[b]:off[b] + cnt[b]].tolist() for b in range(self.sizes.B)]
+
+    def trace_actions(self):
+        """Per group: the taken candidates in order (-1 = STOP)."""
+        tr = self.trace.cpu().numpy()
+        taken = tr[..., 0].view(np.int32)
+        out = []
+        for g in range(self.sizes.G):
+            seq = []
+            for t in range(self.trace_steps):
+                a = int(taken[g, t])
+                if a == -2:
+                    break
+                seq.append(a)
+            out.append(seq)
+        return out

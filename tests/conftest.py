@@ -8,6 +8,16 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 
+def _ensure_library():
+    lib = os.path.join(ROOT, "paper_2609_13804_amd", "libstepprune.so")
+    if not os.path.exists(lib):
+        from paper_2609_13804_amd import build
+        build.build()
+
+
+_ensure_library()
+
+
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
 

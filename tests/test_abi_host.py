@@ -1,0 +1,121 @@
+"""The C ABI on the host: the library loads, exports every entry point the
+header declares, and rejects invalid arguments before any device work.
+
+Every call here fails host-side validation, so no GPU is needed: the
+pointers passed are fake (never dereferenced) and the stream is 0.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "stepprune.h")
+
+
+@pytest.fixture(scope="module")
+def sp():
+    from paper_2609_13804_amd import binding
+    return binding
+
+
+def test_header_symbols_are_exported(sp):
+    text = open(HEADER).read()
+    declared = set(re.findall(r"\b(stepprune_\w+)\s*\(", text))
+    assert declared == set(sp.EXPORTS)
+    lib = sp.library()
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(sp):
+    for code in range(6):
+        assert sp.status_string(code) != "unknown status"
+    assert sp.status_string(99) == "unknown status"
+
+
+FAKE = 0x10000          # aligned, never dereferenced
+MISALIGNED = 0x10008
+
+
+def _dims(sp, d=256, dt=256, h=128, dtype=None):
+    return sp.dims(d, dt, h, sp.SP_BF16 if dtype is None else dtype)
+
+
+def test_workspace_bytes(sp):
+    dm = _dims(sp)
+    assert sp.stepprune_workspace_bytes(0, dm, 100, 10, 2, 3, 50, 10) >= 256 + 10 * 128 * 4
+    sel = sp.stepprune_workspace_bytes(1, dm, 100, 10, 2, 3, 50, 10)
+    assert sel >= 256 + 3 * 2 * 51 * 52 * 4
+    assert sp.stepprune_workspace_bytes(2, dm, 100, 10, 2, 3, 50, 10) == 256
+    assert sp.stepprune_workspace_bytes(1, dm, 100, 10, 2, 3, 5000, 10) == 0   # group too large
+    assert sp.stepprune_workspace_bytes(3, dm, 100, 10, 2, 3, 50, 10) == 0
+    assert sp.stepprune_workspace_bytes(0, _dims(sp, h=100), 100, 10, 2, 3, 50, 10) == 0
+
+
+def _project(sp, dm=None, **kw):
+    args = dict(X=FAKE, T_vis=10, s_start=FAKE, s_stop=FAKE, W_kqv=FAKE, E_text=FAKE,
+                text_off=FAKE, B=1, T_txt=4, W_text=FAKE, g_text=1.0, ln_eps=1e-5, KQV=FAKE,
+                ctx=FAKE, ws=FAKE, ws_bytes=0)
+    args.update(kw)
+    return sp.stepprune_project(dm or _dims(sp), stream=0, raise_on_error=False, **args)
+
+
+def test_project_validation(sp):
+    assert _project(sp, _dims(sp, h=96)) == sp.SP_EINVAL                 # h not a multiple of 64
+    assert _project(sp, _dims(sp, d=0)) == sp.SP_EINVAL
+    assert _project(sp, _dims(sp, dtype=7)) == sp.SP_EUNSUPPORTED
+    assert _project(sp, _dims(sp, h=2048)) == sp.SP_EUNSUPPORTED
+    assert _project(sp, X=None) == sp.SP_EINVAL
+    assert _project(sp, KQV=None) == sp.SP_EINVAL
+    assert _project(sp, W_kqv=MISALIGNED) == sp.SP_EINVAL
+    assert _project(sp, B=0) == sp.SP_EINVAL
+    assert _project(sp, ln_eps=-1.0) == sp.SP_EINVAL
+    assert _project(sp) == sp.SP_EWORKSPACE                              # ws_bytes = 0
+
+
+def _select(sp, dm=None, **kw):
+    args = dict(KQV=FAKE, ctx=FAKE, T_vis=10, img_off=FAKE, B=1, grp_off=FAKE, grp_img=FAKE,
+                grp_cap=FAKE, G=1, max_group=10, max_cap=4, kept_off=FAKE, b_stop=0.0, g=1,
+                flags=0, kept_idx=FAKE, kept_cnt=FAKE, grp_cnt=None, trace=None, trace_steps=0,
+                ws=FAKE, ws_bytes=0)
+    args.update(kw)
+    return sp.stepprune_select(dm or _dims(sp), stream=0, raise_on_error=False, **args)
+
+
+def test_select_validation(sp):
+    assert _select(sp, g=0) == sp.SP_EINVAL
+    assert _select(sp, g=5) == sp.SP_EUNSUPPORTED
+    assert _select(sp, max_group=1023) == sp.SP_EUNSUPPORTED
+    assert _select(sp, max_group=-1) == sp.SP_EINVAL
+    assert _select(sp, flags=8) == sp.SP_EINVAL
+    assert _select(sp, flags=sp.SP_TRACE, trace_steps=5, trace=None) == sp.SP_EINVAL
+    assert _select(sp, b_stop=float("nan")) == sp.SP_EINVAL
+    assert _select(sp, KQV=None) == sp.SP_EINVAL
+    assert _select(sp, grp_off=None) == sp.SP_EINVAL
+    assert _select(sp, ws=MISALIGNED) == sp.SP_EINVAL
+    assert _select(sp, B=0) == sp.SP_EINVAL
+    assert _select(sp) == sp.SP_EWORKSPACE
+
+
+def _compact(sp, dm=None, **kw):
+    args = dict(X=FAKE, img_off=FAKE, E_text=FAKE, text_off=FAKE, kept_idx=FAKE, kept_off=FAKE,
+                kept_cnt=FAKE, B=2, layout=sp.SP_LAYOUT_PADDED, rows_per_image=8, out_rows=16,
+                out=FAKE, seq_info=FAKE, ws=FAKE, ws_bytes=0)
+    args.update(kw)
+    return sp.stepprune_compact(dm or _dims(sp), stream=0, raise_on_error=False, **args)
+
+
+def test_compact_validation(sp):
+    assert _compact(sp, _dims(sp, d=256, dt=128)) == sp.SP_EUNSUPPORTED   # text rows must match
+    assert _compact(sp, layout=7) == sp.SP_EINVAL
+    assert _compact(sp, rows_per_image=9) == sp.SP_EINVAL               # 2 * 9 > out_rows
+    assert _compact(sp, out=None) == sp.SP_EINVAL
+    assert _compact(sp, out=MISALIGNED) == sp.SP_EINVAL
+    assert _compact(sp) == sp.SP_EWORKSPACE
+
+
+def test_read_device_error_rejects_null(sp):
+    code = ctypes.c_int32(0)
+    assert sp.library().stepprune_read_device_error(None, None, ctypes.byref(code)) == sp.SP_EINVAL
