@@ -1,0 +1,252 @@
+#!/usr/bin/env python3
+"""Throughput of StepPrune's inference-time selection path on one MI355X.
+
+One step is the whole path (Algorithm 1) over one batch already resident in
+HBM: stepprune_project (projection GEMM + text context), stepprune_select
+(per-group Gram products + the pointer recurrence with STOP) and
+stepprune_compact (gather into the prefill buffer).  The default batch is
+the LLaVA-1.5-shaped one: 16 images x 576 tokens x 4096, bf16, selector
+hidden width 1024, cap 192, STOP bias set so that the mean retained count is
+about 64, compaction into 576 + 64 prefill rows.
+
+Prints one JSON line.  The roofline object covers the kernel with the largest
+average duration, timed with HIP events that the library records around it
+on the launch stream; the CPU baseline is the float64 oracle timed on this
+host's cores over a bounded sample of the same batch.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload llava15_bf16]
+"""
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "images/sec and µs/image through selector+compaction (N=576, bf16), % roofline"
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix
+PEAK_F32_MATRIX_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+# float32 FMA without packed instructions: 256 CU x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz
+PEAK_F32_VALU_TFLOPS = 78.6
+
+
+class HipEvents:
+    """Raw hipEvent_t handles through libamdhip64 (the library records them on the
+    stream it launches on)."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self):
+        ev = ctypes.c_void_p()
+        if self.hip.hipEventCreate(ctypes.byref(ev)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        return ev.value
+
+    def record(self, ev, stream):
+        if self.hip.hipEventRecord(ev, stream) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def ms(self, a, b):
+        out = ctypes.c_float()
+        if self.hip.hipEventElapsedTime(ctypes.byref(out), a, b) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(out.value)
+
+    def destroy(self, ev):
+        self.hip.hipEventDestroy(ev)
+
+
+def _ensure_built():
+    lib = os.path.join(ROOT, "paper_2609_13804_amd", "libstepprune.so")
+    if not os.path.exists(lib):
+        from paper_2609_13804_amd import build
+        build.build()
+
+
+def _episode_steps(caps, sizes, kept):
+    steps = []
+    for c, n, k in zip(caps, sizes, kept):
+        c, n, k = int(c), int(n), int(k)
+        steps.append(k if k == c else k + 1)      # at the cap no STOP step is taken
+    return steps
+
+
+def cpu_baseline(w, lay, b_stop, budget_s):
+    """The oracle (float64 NumPy, as written) over a bounded sample of the batch."""
+    import numpy as np
+    import oracle
+    from paper_2609_13804_amd import workloads as W
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    done = 0
+    elapsed = 0.0
+    chunk = max(1, min(4, w.batch))
+    images = list(range(w.batch))
+    while done < w.batch and elapsed < budget_s:
+        sub = images[done:done + chunk]
+        inp = W.make_inputs(w, sub)
+        sl = W.make_layout(w, sub)
+        t0 = time.perf_counter()
+        KQV = oracle.project(inp["X"], inp["s_start"], inp["s_stop"], inp["W_kqv"], w.dtype)
+        ctx = oracle.text_context(inp["E_text"], sl.text_off, inp["W_text"])
+        res = oracle.select(KQV, ctx, sl.img_off, sl.grp_off, sl.grp_img, sl.grp_cap, b_stop, w.h,
+                            keep_steps=False)
+        if w.d_text == w.d:
+            oracle.compact(inp["X"], sl.img_off, inp["E_text"], sl.text_off, res.kept, w.layout,
+                           sl.rows_per_image, np.zeros((sl.out_rows, w.d)))
+        elapsed += time.perf_counter() - t0
+        done += len(sub)
+    return {"value": done / elapsed, "unit": "images/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{done} of the {w.batch} images of the {w.name} batch, one pass of "
+                      f"project + select + compact in float64 ({elapsed:.1f} s)"}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llava15_bf16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0,
+                    help="seconds of oracle work for the CPU baseline sample")
+    args = ap.parse_args(argv)
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: the selection path shards by image with no "
+              "communication, and this build measures the one-GPU share (--gpus 1).",
+              file=sys.stderr)
+        return 2
+
+    _ensure_built()
+    import numpy as np
+    import torch
+    from paper_2609_13804_amd import workloads as W
+    from paper_2609_13804_amd.runner import DeviceRun
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    torch.cuda.set_device(0)
+    w = W.WORKLOADS[args.workload]
+    lay = W.make_layout(w)
+    b_stop = W.stop_bias(w)
+    inp = W.make_inputs(w)
+    run = DeviceRun(w, inp, lay, b_stop)
+    del inp
+    stream = torch.cuda.current_stream().cuda_stream
+    hip = HipEvents()
+
+    for _ in range(args.warmup):
+        run.run()
+    torch.cuda.synchronize()
+    if any(run.device_errors()):
+        raise RuntimeError(f"device error words {run.device_errors()}")
+
+    K = args.steps
+    names = ["step0", "proj0", "proj1", "projd", "gram0", "gram1", "rec0", "rec1", "seld",
+             "gath0", "gath1", "step1"]
+    evs = [{n: hip.create() for n in names} for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        e = evs[k]
+        hip.record(e["step0"], stream)
+        run.project(stream, events=[e["proj0"], e["proj1"]])
+        hip.record(e["projd"], stream)
+        run.select(stream, events=[e["gram0"], e["gram1"], e["rec0"], e["rec1"]])
+        hip.record(e["seld"], stream)
+        run.compact(stream, events=[e["gath0"], e["gath1"]])
+        hip.record(e["step1"], stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    if any(run.device_errors()):
+        raise RuntimeError(f"device error words {run.device_errors()}")
+
+    def avg_us(a, b):
+        return 1e3 * sum(hip.ms(e[a], e[b]) for e in evs) / K
+
+    stages = {"project": avg_us("step0", "projd"), "select": avg_us("projd", "seld"),
+              "compact": avg_us("seld", "step1"), "step": avg_us("step0", "step1")}
+    kernels = {"project_gemm": avg_us("proj0", "proj1"), "gram_gemm": avg_us("gram0", "gram1"),
+               "select_recurrence": avg_us("rec0", "rec1"), "compact_gather": avg_us("gath0", "gath1")}
+    for e in evs:
+        for ev in e.values():
+            hip.destroy(ev)
+
+    s = run.sizes
+    sizes = np.diff(lay.grp_off)
+    kept_g = run.grp_cnt.cpu().numpy()[:s.G]
+    kept_b = run.kept_cnt.cpu().numpy()
+    steps_g = _episode_steps(run.caps_host, sizes, kept_g)
+    eb = 2 if w.dtype == "bf16" else 4
+    L = np.diff(lay.text_off)
+
+    work = {
+        "project_gemm": ("mfma", 2.0 * (s.T_vis + 2) * w.d * 3 * w.h * 1e-12,
+                         PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_MATRIX_TFLOPS, "TFLOP/s"),
+        "gram_gemm": ("mfma", sum(2.0 * 2 * (n + 1) * (n + 2) * w.h for n in sizes) * 1e-12,
+                      PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_MATRIX_TFLOPS, "TFLOP/s"),
+        "select_recurrence": ("alu", sum(2.0 * (n + 1) * st * (st + 1) / 2
+                                         for n, st in zip(sizes, steps_g)) * 1e-12,
+                              PEAK_F32_VALU_TFLOPS, "TFLOP/s"),
+        "compact_gather": ("hbm", float(((kept_b + L) * w.d * eb * 2).sum() + kept_b.sum() * 4) * 1e-9,
+                           PEAK_HBM_GBS, "GB/s"),
+    }
+    dom = max(kernels, key=kernels.get)
+    bound, amount, peak, unit = work[dom]
+    achieved = amount / (kernels[dom] * 1e-6)
+    roofline = {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": unit,
+                "frac": round(achieved / peak, 4), "traffic": None, "kernel": dom,
+                "algorithmic": f"{amount:.6g} {'TFLOP' if unit == 'TFLOP/s' else 'GB'} per launch"}
+
+    elapsed = t1 - t0
+    value = K * s.B / elapsed
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(1e3 * elapsed / K, 4),
+        "us_per_image": round(1e6 * elapsed / (K * s.B), 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "images": s.B, "groups": s.G,
+                   "tokens": int(s.T_vis), "d": w.d, "h": w.h, "text_tokens": int(s.T_txt),
+                   "layout": w.layout, "b_stop": b_stop,
+                   "kept_mean_per_image": round(float(kept_b.mean()), 3),
+                   "selection_steps": int(sum(steps_g)),
+                   "longest_episode_steps": int(max(steps_g))},
+        "stages_us": {k: round(v, 2) for k, v in stages.items()},
+        "kernels_us": {k: round(v, 2) for k, v in kernels.items()},
+        "selection_steps_per_s": round(sum(steps_g) / (stages["select"] * 1e-6), 1),
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, lay, b_stop, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

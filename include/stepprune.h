@@ -30,6 +30,13 @@
  *    recorded in a device error word inside `ws`; the affected outputs are
  *    then undefined.  stepprune_read_device_error() reads it.
  *  - No C++ exception crosses this interface.
+ *  - `events` (host) is NULL or points to caller-created hipEvent_t handles that
+ *    the call records on `stream` around its main kernels, for timing:
+ *      project: [0] before, [1] after the projection GEMM;
+ *      select:  [0] before, [1] after the Gram products, [2] before, [3] after
+ *               the pointer recurrence;
+ *      compact: [0] before, [1] after the gather.
+ *    A NULL entry is skipped.  The library neither creates nor destroys events.
  *
  * Numerics: projections accumulate in float32 and are stored once, rounded to
  * nearest-even, in the dtype of sp_dims (bfloat16 or float32); the text context
@@ -113,7 +120,8 @@ sp_status stepprune_project(const sp_dims* dims,
                             int32_t B, int64_t T_txt,
                             const void* W_text, float g_text, float ln_eps,
                             void* KQV, float* ctx,
-                            void* ws, size_t ws_bytes, hipStream_t stream);
+                            void* ws, size_t ws_bytes,
+                            const hipEvent_t* events, hipStream_t stream);
 
 /*
  * Algorithm 1 steps 2-4 (Eq. 2, Eq. 4).  Every group (a contiguous run of one
@@ -156,7 +164,8 @@ sp_status stepprune_select(const sp_dims* dims,
                            float b_stop, int32_t g, uint32_t flags,
                            int32_t* kept_idx, int32_t* kept_cnt, int32_t* grp_cnt,
                            float* trace, int32_t trace_steps,
-                           void* ws, size_t ws_bytes, hipStream_t stream);
+                           void* ws, size_t ws_bytes,
+                           const hipEvent_t* events, hipStream_t stream);
 
 /*
  * Algorithm 1 step 5.  Gathers each image's kept visual rows (ascending) and
@@ -177,7 +186,8 @@ sp_status stepprune_compact(const sp_dims* dims,
                             const int32_t* kept_cnt, int32_t B,
                             int32_t layout, int32_t rows_per_image, int64_t out_rows,
                             void* out, int32_t* seq_info,
-                            void* ws, size_t ws_bytes, hipStream_t stream);
+                            void* ws, size_t ws_bytes,
+                            const hipEvent_t* events, hipStream_t stream);
 
 /* Workspace bytes for stage `which` (0 project, 1 select, 2 compact) at the
    given sizes (host).  Returns 0 for invalid arguments. */

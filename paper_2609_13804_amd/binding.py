@@ -48,13 +48,13 @@ _DIMS = ctypes.POINTER(sp_dims)
 
 _lib.stepprune_project.restype = _I32
 _lib.stepprune_project.argtypes = [_DIMS, _P, _I64, _P, _P, _P, _P, _P, _I32, _I64, _P, _F32, _F32,
-                                   _P, _P, _P, _SZ, _P]
+                                   _P, _P, _P, _SZ, _P, _P]
 _lib.stepprune_select.restype = _I32
 _lib.stepprune_select.argtypes = [_DIMS, _P, _P, _I64, _P, _I32, _P, _P, _P, _I32, _I32, _I32, _P,
-                                  _F32, _I32, ctypes.c_uint32, _P, _P, _P, _P, _I32, _P, _SZ, _P]
+                                  _F32, _I32, ctypes.c_uint32, _P, _P, _P, _P, _I32, _P, _SZ, _P, _P]
 _lib.stepprune_compact.restype = _I32
 _lib.stepprune_compact.argtypes = [_DIMS, _P, _P, _P, _P, _P, _P, _P, _I32, _I32, _I32, _I64, _P, _P,
-                                   _P, _SZ, _P]
+                                   _P, _SZ, _P, _P]
 _lib.stepprune_workspace_bytes.restype = _SZ
 _lib.stepprune_workspace_bytes.argtypes = [_I32, _DIMS, _I64, _I64, _I32, _I32, _I32, _I32]
 _lib.stepprune_read_device_error.restype = _I32
@@ -73,6 +73,14 @@ def _ptr(t) -> Optional[int]:
     if isinstance(t, int):
         return t
     return t.data_ptr()
+
+
+def _events(events):
+    """None, or a sequence of raw hipEvent_t handles (ints, 0 = skip)."""
+    if events is None:
+        return None
+    arr = (ctypes.c_void_p * len(events))(*[e or None for e in events])
+    return ctypes.cast(arr, ctypes.c_void_p)
 
 
 def _stream(stream) -> Optional[int]:
@@ -104,32 +112,33 @@ def stepprune_workspace_bytes(which, dm, T_vis, T_txt, B, G, max_group, max_cap)
 
 
 def stepprune_project(dm, X, T_vis, s_start, s_stop, W_kqv, E_text, text_off, B, T_txt, W_text,
-                      g_text, ln_eps, KQV, ctx, ws, ws_bytes, stream=None, raise_on_error=True):
+                      g_text, ln_eps, KQV, ctx, ws, ws_bytes, stream=None, raise_on_error=True,
+                      events=None):
     st = _lib.stepprune_project(ctypes.byref(dm), _ptr(X), T_vis, _ptr(s_start), _ptr(s_stop),
                                 _ptr(W_kqv), _ptr(E_text), _ptr(text_off), B, T_txt, _ptr(W_text),
                                 g_text, ln_eps, _ptr(KQV), _ptr(ctx), _ptr(ws), ws_bytes,
-                                _stream(stream))
+                                _events(events), _stream(stream))
     return _check("stepprune_project", st, raise_on_error)
 
 
 def stepprune_select(dm, KQV, ctx, T_vis, img_off, B, grp_off, grp_img, grp_cap, G, max_group,
                      max_cap, kept_off, b_stop, g, flags, kept_idx, kept_cnt, grp_cnt, trace,
-                     trace_steps, ws, ws_bytes, stream=None, raise_on_error=True):
+                     trace_steps, ws, ws_bytes, stream=None, raise_on_error=True, events=None):
     st = _lib.stepprune_select(ctypes.byref(dm), _ptr(KQV), _ptr(ctx), T_vis, _ptr(img_off), B,
                                _ptr(grp_off), _ptr(grp_img), _ptr(grp_cap), G, max_group, max_cap,
                                _ptr(kept_off), b_stop, g, flags, _ptr(kept_idx), _ptr(kept_cnt),
                                _ptr(grp_cnt), _ptr(trace), trace_steps, _ptr(ws), ws_bytes,
-                               _stream(stream))
+                               _events(events), _stream(stream))
     return _check("stepprune_select", st, raise_on_error)
 
 
 def stepprune_compact(dm, X, img_off, E_text, text_off, kept_idx, kept_off, kept_cnt, B, layout,
                       rows_per_image, out_rows, out, seq_info, ws, ws_bytes, stream=None,
-                      raise_on_error=True):
+                      raise_on_error=True, events=None):
     st = _lib.stepprune_compact(ctypes.byref(dm), _ptr(X), _ptr(img_off), _ptr(E_text),
                                 _ptr(text_off), _ptr(kept_idx), _ptr(kept_off), _ptr(kept_cnt), B,
                                 layout, rows_per_image, out_rows, _ptr(out), _ptr(seq_info),
-                                _ptr(ws), ws_bytes, _stream(stream))
+                                _ptr(ws), ws_bytes, _events(events), _stream(stream))
     return _check("stepprune_compact", st, raise_on_error)
 
 

@@ -17,6 +17,9 @@ LIB = os.path.join(HERE, "libstepprune.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
 SOURCES = ["api.hip", "gemm.hip", "select.hip", "text.hip", "compact.hip"]
+# The selection recurrence keeps each column's history in vector registers; let
+# alloca promotion use the whole VGPR budget instead of a quarter of it.
+EXTRA_FLAGS = {"select.hip": ["-mllvm", "-amdgpu-promote-alloca-to-vector-vgpr-ratio=1"]}
 ARCH = "gfx950"
 # Packed fp32 ALU ops are disabled for every translation unit.
 HIPCC_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
@@ -52,7 +55,8 @@ def build(jobs: int = 8, verbose: bool = False) -> str:
     for src in SOURCES:
         obj = os.path.join(BUILD_DIR, src.replace(".hip", ".o"))
         objs.append(obj)
-        cmds.append([hipcc, *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        cmds.append([hipcc, *HIPCC_FLAGS, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src),
+                     "-o", obj])
     with concurrent.futures.ThreadPoolExecutor(max_workers=max(1, jobs)) as ex:
         list(ex.map(lambda c: _run(c, verbose), cmds))
     tmp = LIB + ".tmp"

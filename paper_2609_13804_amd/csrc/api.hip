@@ -85,7 +85,7 @@ sp_status stepprune_project(const sp_dims* dims, const void* X, int64_t T_vis, c
                             const void* s_stop, const void* W_kqv, const void* E_text,
                             const int32_t* text_off, int32_t B, int64_t T_txt, const void* W_text,
                             float g_text, float ln_eps, void* KQV, float* ctx, void* ws,
-                            size_t ws_bytes, hipStream_t stream) {
+                            size_t ws_bytes, const hipEvent_t* events, hipStream_t stream) {
   sp_status st = check_dims(dims);
   if (st != SP_OK) return st;
   if (T_vis < 0 || T_txt < 0 || B < 1) return SP_EINVAL;
@@ -101,9 +101,11 @@ sp_status stepprune_project(const sp_dims* dims, const void* X, int64_t T_vis, c
   int32_t* err = reinterpret_cast<int32_t*>(ws);
   float* tproj = reinterpret_cast<float*>(static_cast<char*>(ws) + kWsHeaderBytes);
   hipError_t e = launch_clear_error(err, stream);
+  record_event(events, 0, stream);
   if (e == hipSuccess)
     e = launch_project_gemm(dims->dtype, X, T_vis, s_start, s_stop, W_kqv, dims->d, 3 * dims->h,
                             KQV, stream);
+  record_event(events, 1, stream);
   if (e == hipSuccess)
     e = launch_text_gemm(dims->dtype, E_text, T_txt, W_text, dims->d_text, dims->h, tproj, stream);
   if (e == hipSuccess)
@@ -117,7 +119,8 @@ sp_status stepprune_select(const sp_dims* dims, const void* KQV, const float* ct
                            int32_t max_group, int32_t max_cap, const int32_t* kept_off,
                            float b_stop, int32_t g, uint32_t flags, int32_t* kept_idx,
                            int32_t* kept_cnt, int32_t* grp_cnt, float* trace, int32_t trace_steps,
-                           void* ws, size_t ws_bytes, hipStream_t stream) {
+                           void* ws, size_t ws_bytes, const hipEvent_t* events,
+                           hipStream_t stream) {
   sp_status st = check_dims(dims);
   if (st != SP_OK) return st;
   if (T_vis < 0 || B < 1 || G < 0 || max_group < 0 || max_cap < 0 || trace_steps < 0)
@@ -165,6 +168,7 @@ sp_status stepprune_select(const sp_dims* dims, const void* KQV, const float* ct
   a.grp_kept = reinterpret_cast<int32_t*>(wsb + lay.kept);
   a.grp_count = reinterpret_cast<int32_t*>(wsb + lay.count);
   a.err = reinterpret_cast<int32_t*>(wsb);
+  a.events = events;
   hipError_t e = launch_clear_error(a.err, stream);
   if (e == hipSuccess) e = launch_select(a, stream);
   return hip_status(e);
@@ -174,7 +178,8 @@ sp_status stepprune_compact(const sp_dims* dims, const void* X, const int32_t* i
                             const void* E_text, const int32_t* text_off, const int32_t* kept_idx,
                             const int32_t* kept_off, const int32_t* kept_cnt, int32_t B,
                             int32_t layout, int32_t rows_per_image, int64_t out_rows, void* out,
-                            int32_t* seq_info, void* ws, size_t ws_bytes, hipStream_t stream) {
+                            int32_t* seq_info, void* ws, size_t ws_bytes,
+                            const hipEvent_t* events, hipStream_t stream) {
   sp_status st = check_dims(dims);
   if (st != SP_OK) return st;
   if (dims->d_text != dims->d) return SP_EUNSUPPORTED;
@@ -205,7 +210,9 @@ sp_status stepprune_compact(const sp_dims* dims, const void* X, const int32_t* i
   a.seq_info = seq_info;
   a.err = reinterpret_cast<int32_t*>(ws);
   hipError_t e = launch_clear_error(a.err, stream);
+  record_event(events, 0, stream);
   if (e == hipSuccess) e = launch_compact(a, stream);
+  record_event(events, 1, stream);
   return hip_status(e);
 }
 

@@ -11,9 +11,11 @@
 // and the history scores are sigma A[e, col(tau)].  A and B are dense
 // contractions computed once per group on the matrix cores (gemm.hip), so a
 // step needs only the rows A[e, :] and B[e, :] of the newest history entry e:
-// one dependent load, then O(t * n) float32 FMAs over history rows kept in
-// LDS.  One workgroup runs one episode end to end, thread j owning candidate
-// column j (j = n is STOP), so no step ever leaves the compute unit.
+// one dependent load, then O(t * n) float32 FMAs.  One workgroup runs one
+// episode end to end, thread j owning candidate column j (j = n is STOP), so
+// no step ever leaves the compute unit: each thread keeps its column of the
+// history B rows in registers (LDS past RREG entries), every wave computes the
+// history softmax itself, reductions use DPP, and a step costs two barriers.
 //
 // Gram layout per group (float32, row stride ld): rows [0, n) A rows of the
 // tokens, row n the A row of START, rows [n+1, 2n+1) B rows of the tokens,
@@ -25,53 +27,6 @@ namespace {
 
 constexpr int kMaxWaves = 16;
 
-// Dynamic LDS of the selection kernel (byte offsets), shared by host and device.
-struct SelLds {
-  int hist, arow, hrow, alpha, red, stop, total;
-  __host__ __device__ SelLds(int rows, int hist_ld, int max_cap) {
-    hist = 0;
-    arow = hist + rows * hist_ld * 4;
-    hrow = arow + (hist_ld + 4) * 4;
-    alpha = hrow + (max_cap + 1) * 4;
-    red = (alpha + (max_cap + 1) * 4 + 15) & ~15;
-    stop = red + 2 * kMaxWaves * 8;
-    total = stop + 16;
-  }
-};
-
-// Order-preserving key: larger value wins, equal values go to the lower index.
-__device__ inline uint64_t make_key(float v, int idx) {
-  uint32_t u = __float_as_uint(v);
-  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-  return ((uint64_t)u << 32) | (uint32_t)(~(uint32_t)idx);
-}
-__device__ inline int key_index(uint64_t k) { return (int)(~(uint32_t)(k & 0xffffffffu)); }
-__device__ inline float key_value(uint64_t k) {
-  uint32_t u = (uint32_t)(k >> 32);
-  u = (u & 0x80000000u) ? (u & 0x7fffffffu) : ~u;
-  return __uint_as_float(u);
-}
-
-__device__ inline uint64_t shfl_xor_u64(uint64_t v, int m) {
-  uint32_t lo = __shfl_xor((uint32_t)v, m, 64);
-  uint32_t hi = __shfl_xor((uint32_t)(v >> 32), m, 64);
-  return ((uint64_t)hi << 32) | lo;
-}
-
-// Keys are unique (they carry the index) or zero (no candidate).
-__device__ inline void top2_merge(uint64_t& a1, uint64_t& a2, uint64_t b1, uint64_t b2) {
-  const uint64_t hi = a1 > b1 ? a1 : b1;
-  const uint64_t lo = a1 > b1 ? b1 : a1;
-  uint64_t second = lo > a2 ? lo : a2;
-  second = second > b2 ? second : b2;
-  a1 = hi;
-  a2 = second;
-}
-
-__device__ inline float wave_max(float v) {
-  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
-  return v;
-}
 __device__ inline float wave_sum(float v) {
   for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
   return v;
@@ -112,6 +67,45 @@ __global__ __launch_bounds__(256) void ck_kernel(const T* __restrict__ KQV, int6
 
 // ------------------------------------------------------------------ the recurrence
 
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ inline float dpp_mov(float old, float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(v), CTRL,
+                                                    ROW_MASK, 0xf, false));
+}
+
+// Wave-wide max / sum with DPP row shifts and row broadcasts (result in lane 63,
+// returned to every lane); a fixed combination order, so results are deterministic.
+__device__ inline float wave_max_dpp(float v) {
+  v = fmaxf(v, dpp_mov<0x111>(-INFINITY, v));        // row_shr:1
+  v = fmaxf(v, dpp_mov<0x112>(-INFINITY, v));        // row_shr:2
+  v = fmaxf(v, dpp_mov<0x114>(-INFINITY, v));        // row_shr:4
+  v = fmaxf(v, dpp_mov<0x118>(-INFINITY, v));        // row_shr:8
+  v = fmaxf(v, dpp_mov<0x142, 0xa>(-INFINITY, v));   // row_bcast:15
+  v = fmaxf(v, dpp_mov<0x143, 0xc>(-INFINITY, v));   // row_bcast:31
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+__device__ inline float wave_sum_dpp(float v) {
+  v += dpp_mov<0x111>(0.0f, v);
+  v += dpp_mov<0x112>(0.0f, v);
+  v += dpp_mov<0x114>(0.0f, v);
+  v += dpp_mov<0x118>(0.0f, v);
+  v += dpp_mov<0x142, 0xa>(0.0f, v);
+  v += dpp_mov<0x143, 0xc>(0.0f, v);
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+typedef float f32x32_t __attribute__((ext_vector_type(32)));
+
+__device__ inline int wave_min_dpp(int v) {
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x111, 0xf, 0xf, false));
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x112, 0xf, 0xf, false));
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x114, 0xf, 0xf, false));
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x118, 0xf, 0xf, false));
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x142, 0xa, 0xf, false));
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x143, 0xc, 0xf, false));
+  return __builtin_amdgcn_readlane(v, 63);
+}
+
 struct SelParams {
   const float* gram;
   int64_t gstride;
@@ -126,8 +120,8 @@ struct SelParams {
   int64_t T_vis;
   int max_group;
   int max_cap;
-  int hist_lds_rows;   // history rows held in LDS; older ones read from the Gram buffer
-  int hist_ld;         // LDS row stride (floats)
+  int lds_tier;        // history entries per column held in LDS after the registers
+  int alpha_ld;        // softmax weight array length (floats, multiple of 16)
   float sigma;
   float b_stop;
   uint32_t flags;
@@ -139,8 +133,28 @@ struct SelParams {
   int32_t* err;
 };
 
-template <bool TRACE>
-__global__ __launch_bounds__(1024) void select_kernel(SelParams p) {
+// Dynamic LDS of the recurrence (byte offsets), shared by host and device.
+// The LDS history tier is column-major, [column][lds_tier], so one 16-byte
+// read gives a thread four consecutive history entries of its column.
+struct SelLds {
+  int hist, arow, hcol, alpha, red, stop, total;
+  __host__ __device__ SelLds(int lds_tier, int max_group, int max_cap, int alpha_ld) {
+    hist = 0;
+    arow = hist + (max_group + 1) * lds_tier * 4;
+    hcol = arow + ((max_group + 2 + 3) & ~3) * 4;
+    alpha = (hcol + (max_cap + 2) * 4 + 15) & ~15;
+    red = alpha + alpha_ld * 4;
+    stop = red + kMaxWaves * 16;
+    total = stop + 16;
+  }
+};
+
+// One workgroup runs one episode.  Thread j owns candidate column j (j = n is
+// STOP, j = n + 1 only loads the START column of A rows).  History B values of
+// its column: the first RREG in registers, the next lds_tier in LDS, any
+// further ones re-read from the Gram buffer in batches.
+template <int NT, int RREG, bool TRACE>
+__global__ __launch_bounds__(NT) void select_kernel(SelParams p) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int g = blockIdx.x;
   const int tid = threadIdx.x;
@@ -167,118 +181,225 @@ __global__ __launch_bounds__(1024) void select_kernel(SelParams p) {
     }
   }
   const bool no_history = (p.flags & SP_NO_HISTORY) != 0;
-  const int R = p.hist_lds_rows;
-  const int HL = p.hist_ld;
+  const int LT = p.lds_tier;
+  const SelLds L(LT, p.max_group, p.max_cap, p.alpha_ld);
+  float* hist = reinterpret_cast<float*>(smem + L.hist);      // [max_group + 1][LT]
+  float* arow = reinterpret_cast<float*>(smem + L.arow);      // A row of the newest entry
+  int* hcol = reinterpret_cast<int*>(smem + L.hcol);          // A column of each history entry
+  float* alpha = reinterpret_cast<float*>(smem + L.alpha);    // softmax weights (zero padded)
+  float4* red = reinterpret_cast<float4*>(smem + L.red);      // per wave {v1, i1, v2, i2}
+  float* stop_sh = reinterpret_cast<float*>(smem + L.stop);
 
-  const SelLds L(R, HL, p.max_cap);
-  float* hist = reinterpret_cast<float*>(smem + L.hist);        // [R][HL] history B rows
-  float* arow = reinterpret_cast<float*>(smem + L.arow);        // [HL + 4] A row of newest entry
-  int* hrow = reinterpret_cast<int*>(smem + L.hrow);            // [max_cap + 1] history rows
-  float* alpha = reinterpret_cast<float*>(smem + L.alpha);      // [max_cap + 1] softmax weights
-  uint64_t* red = reinterpret_cast<uint64_t*>(smem + L.red);    // [2][kMaxWaves] wave maxima
-  float* stop_sh = reinterpret_cast<float*>(smem + L.stop);     // STOP logit (trace)
-
-  const float* A = p.gram + (int64_t)g * p.gstride;        // A row r: A + r * ld
-  const float* Bm = A + (int64_t)(n + 1) * p.ld;           // B row r: Bm + r * ld
+  const float* A = p.gram + (int64_t)g * p.gstride;           // A row r at A + r * ld
+  const float* Bm = A + (int64_t)(n + 1) * p.ld;              // B row r at Bm + r * ld
   const int j = tid;
-  const bool col = j <= n;                                 // owns a candidate column
+  const bool col = j <= n;
   const float ck = col ? p.cK[(int64_t)g * p.ck_ld + j] : 0.0f;
+  const float sigma = p.sigma;
+  float* hist_j = hist + (col ? j : 0) * LT;
 
-  // History entry 0 is START (row n of A and B, column n + 1 of A).
+  // Register-resident history of this column: up to 128 values in four
+  // separate 32-wide vector registers.  Reads use constant slots after
+  // unrolling; a write picks the vector with a uniform branch and the element
+  // with an indexed register move.  Separate variables rather than an array,
+  // and conditions the optimiser cannot prove exclusive, keep every access a
+  // register operation (an aggregate written at a dynamic index would be
+  // placed in scratch memory).
+  static_assert(RREG % 32 == 0 && RREG <= 128, "history registers come in 32-wide vectors");
+  constexpr int NV = RREG / 32;
+  f32x32_t h0{}, h1{}, h2{}, h3{};
+  auto hget = [&](int i) -> float {
+    return i < 32 ? h0[i & 31] : i < 64 ? h1[i & 31] : i < 96 ? h2[i & 31] : h3[i & 31];
+  };
+  auto hput = [&](int pos, float x) {
+    const int e = pos & 31;
+    const int k = pos >> 5;
+    if (__builtin_amdgcn_readfirstlane(k == 0)) h0[e] = x;
+    if (NV > 1 && __builtin_amdgcn_readfirstlane(k == 1)) h1[e] = x;
+    if (NV > 2 && __builtin_amdgcn_readfirstlane(k == 2)) h2[e] = x;
+    if (NV > 3 && __builtin_amdgcn_readfirstlane(k == 3)) h3[e] = x;
+  };
+  // A column of history entry lane + 64 k, for the first 256 entries.
+  int hc0 = lane == 0 ? n + 1 : 0, hc1 = 0, hc2 = 0, hc3 = 0;
+
+  // History entry 0 is START: row n of A and B, column n + 1 of A.
   if (j <= n + 1) arow[j] = A[(int64_t)n * p.ld + j];
-  if (col) {
-    const float bv = Bm[(int64_t)n * p.ld + j];
-    if (R > 0) hist[j] = bv;
-  }
-  if (tid == 0) hrow[0] = n;
+  h0[0] = col ? Bm[(int64_t)n * p.ld + j] : 0.0f;
+  if (tid == 0) hcol[0] = n + 1;
   bool selected = false;
-  int hlen = 1;
+  int hl = 1;       // history length
   int kept = 0;
   __syncthreads();
 
   for (int t = 1; t <= cap; ++t) {
-    // Softmax weights of the history (one wave).
-    if (wave == 0) {
+    // ---- softmax of sigma * A[e, history]; every wave computes the same
+    // weights and writes the same values to the shared array, reading back only
+    // what it wrote itself.
+    const int hpad = (hl + 15) & ~15;
+    if (hl <= 256) {
+      float sv[4];
       float m = -INFINITY;
-      for (int tau = lane; tau < hlen; tau += 64) {
-        const int r = hrow[tau];
-        const float s = p.sigma * arow[r == n ? n + 1 : r];
-        alpha[tau] = s;
-        m = fmaxf(m, s);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        sv[k] = -INFINITY;
+        if (64 * k < hl) {
+          const int hc = k == 0 ? hc0 : k == 1 ? hc1 : k == 2 ? hc2 : hc3;
+          if (lane + 64 * k < hl) sv[k] = sigma * arow[hc];
+          m = fmaxf(m, sv[k]);
+        }
       }
-      m = wave_max(m);
+      m = wave_max_dpp(m);
       float sum = 0.0f;
-      for (int tau = lane; tau < hlen; tau += 64) {
-        const float e = expf(alpha[tau] - m);
-        alpha[tau] = e;
-        sum += e;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if (64 * k < hl) {
+          sv[k] = lane + 64 * k < hl ? expf(sv[k] - m) : 0.0f;
+          sum += sv[k];
+        }
       }
-      sum = wave_sum(sum);
-      for (int tau = lane; tau < hlen; tau += 64) alpha[tau] = alpha[tau] / sum;
+      sum = wave_sum_dpp(sum);
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        if (lane + 64 * k < hpad) alpha[lane + 64 * k] = sv[k] / sum;
+    } else {
+      // Longer histories: scores are recomputed in each pass so that only
+      // final weights (identical in every wave) are ever written.
+      float m = -INFINITY;
+      for (int tau = lane; tau < hl; tau += 64) m = fmaxf(m, sigma * arow[hcol[tau]]);
+      m = wave_max_dpp(m);
+      float sum = 0.0f;
+      for (int tau = lane; tau < hl; tau += 64) sum += expf(sigma * arow[hcol[tau]] - m);
+      sum = wave_sum_dpp(sum);
+      for (int tau = lane; tau < hl; tau += 64) alpha[tau] = expf(sigma * arow[hcol[tau]] - m) / sum;
+      if (hl + lane < hpad) alpha[hl + lane] = 0.0f;
     }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+
+    // ---- pointer logit of this thread's candidate
+    float acc = col ? ck + arow[j] : 0.0f;
+#pragma unroll
+    for (int blk = 0; blk < RREG; blk += 16) {
+      if (blk < hl) {
+        const float4* a4 = reinterpret_cast<const float4*>(alpha + blk);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 x = a4[q];
+          acc = fmaf(x.x, hget(blk + 4 * q + 0), acc);
+          acc = fmaf(x.y, hget(blk + 4 * q + 1), acc);
+          acc = fmaf(x.z, hget(blk + 4 * q + 2), acc);
+          acc = fmaf(x.w, hget(blk + 4 * q + 3), acc);
+        }
+      }
+    }
+    if (hl > RREG) {
+      const int lds_end = hl < RREG + LT ? hl : RREG + LT;
+      int tau = RREG;
+      for (; tau + 4 <= lds_end; tau += 4) {
+        const float4 x = *reinterpret_cast<const float4*>(alpha + tau);
+        const float4 y = col ? *reinterpret_cast<const float4*>(hist_j + (tau - RREG))
+                             : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        acc = fmaf(x.x, y.x, acc);
+        acc = fmaf(x.y, y.y, acc);
+        acc = fmaf(x.z, y.z, acc);
+        acc = fmaf(x.w, y.w, acc);
+      }
+      for (; tau < lds_end; ++tau) acc = fmaf(alpha[tau], col ? hist_j[tau - RREG] : 0.0f, acc);
+      for (; tau < hl; tau += 8) {
+        float hv[8], av[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          hv[u] = 0.0f;
+          av[u] = 0.0f;
+          if (tau + u < hl) {
+            const int c = hcol[tau + u];
+            const int r = c == n + 1 ? n : c;
+            av[u] = alpha[tau + u];
+            if (col) hv[u] = Bm[(int64_t)r * p.ld + j];
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc = fmaf(av[u], hv[u], acc);
+      }
+    }
+    float lj = sigma * acc;
+    if (j == n) {
+      lj += p.b_stop;
+      if (TRACE) *stop_sh = lj;
+    }
+    const bool valid = col && !selected;
+
+    // ---- first maximal candidate of this wave (lowest index on ties)
+    const float v = valid ? lj : -INFINITY;
+    const float vmax = wave_max_dpp(v);
+    const uint64_t mask = __ballot(valid && v == vmax);
+    const int i1 = mask ? wave * 64 + __ffsll((unsigned long long)mask) - 1 : -1;
+    float v2 = -INFINITY;
+    int i2 = -1;
+    if (TRACE) {
+      const bool keep = valid && j != i1;
+      const float w2 = keep ? lj : -INFINITY;
+      v2 = wave_max_dpp(w2);
+      const uint64_t mask2 = __ballot(keep && w2 == v2);
+      i2 = mask2 ? wave * 64 + __ffsll((unsigned long long)mask2) - 1 : -1;
+    }
+    if (lane == 0) red[wave] = make_float4(vmax, __int_as_float(i1), v2, __int_as_float(i2));
     __syncthreads();
 
-    // Pointer logits of this thread's candidate.
-    uint64_t k1 = 0, k2 = 0;
-    float lj = 0.0f;
-    if (col && !selected) {
-      float acc = ck + arow[j];
-      const int nl = hlen < R ? hlen : R;
-      for (int tau = 0; tau < nl; ++tau) acc = fmaf(alpha[tau], hist[tau * HL + j], acc);
-      for (int tau = nl; tau < hlen; ++tau)
-        acc = fmaf(alpha[tau], Bm[(int64_t)hrow[tau] * p.ld + j], acc);
-      lj = p.sigma * acc;
-      if (j == n) {
-        lj += p.b_stop;
-        if (TRACE) *stop_sh = lj;
-      }
-      k1 = make_key(lj, j);
+    // ---- merge the waves' candidates with one wave-wide reduction: lane w
+    // holds wave w's best (lanes 16 + w its runner-up); largest value, then
+    // lowest index.
+    float cv = -INFINITY;
+    int ci = -1;
+    if (lane < nwaves) {
+      const float4 r = red[lane];
+      cv = r.x;
+      ci = __float_as_int(r.y);
+    } else if (TRACE && lane >= 16 && lane < 16 + nwaves) {
+      const float4 r = red[lane - 16];
+      cv = r.z;
+      ci = __float_as_int(r.w);
     }
-    // First maximal candidate over the group (STOP has the largest index, so
-    // it loses exact ties).
-    for (int m = 32; m >= 1; m >>= 1) {
-      const uint64_t o1 = shfl_xor_u64(k1, m);
-      if (TRACE) {
-        const uint64_t o2 = shfl_xor_u64(k2, m);
-        top2_merge(k1, k2, o1, o2);
-      } else {
-        k1 = k1 > o1 ? k1 : o1;
-      }
-    }
-    if (lane == 0) {
-      red[wave] = k1;
-      if (TRACE) red[kMaxWaves + wave] = k2;
-    }
-    __syncthreads();
-    uint64_t best = 0, second = 0;
-    for (int w = 0; w < nwaves; ++w) {
-      if (TRACE) top2_merge(best, second, red[w], red[kMaxWaves + w]);
-      else best = best > red[w] ? best : red[w];
-    }
-    const int a = key_index(best);       // best != 0: STOP always competes
-    if (TRACE && tid == 0 && t <= p.trace_steps) {
+    const float bv = wave_max_dpp(ci >= 0 ? cv : -INFINITY);
+    const int a = wave_min_dpp(ci >= 0 && cv == bv ? ci : INT_MAX);   // STOP always competes
+    if (TRACE) {
+      // Runner-up over the same lanes (whole wave active for the reductions).
+      const bool rest = ci >= 0 && ci != a;
+      const float sv2 = wave_max_dpp(rest ? cv : -INFINITY);
+      const int si2 = wave_min_dpp(rest && cv == sv2 ? ci : INT_MAX);
+      if (tid == 0 && t <= p.trace_steps) {
       float* rec = p.trace + ((int64_t)g * p.trace_steps + (t - 1)) * 4;
       rec[0] = __int_as_float(a == n ? -1 : a);
-      rec[1] = key_value(best);
-      rec[2] = second ? key_value(second) : -INFINITY;
+      rec[1] = bv;
+      rec[2] = si2 != INT_MAX ? sv2 : -INFINITY;
       rec[3] = *stop_sh;
+      }
     }
     if (a == n) break;
     ++kept;
     if (j == a) selected = true;
     if (!no_history) {
-      // Append a to the history: its A row becomes the current row, its B row
-      // the newest history row.
-      if (tid == 0) hrow[hlen] = a;
+      // Append a: its A row becomes the current row, its B row the newest
+      // history entry of every column.
+      if (tid == 0) hcol[hl] = a;
+      {
+        const int k = hl >> 6;
+        const bool mine = lane == (hl & 63);
+        if (__builtin_amdgcn_readfirstlane(k == 0) && mine) hc0 = a;
+        if (__builtin_amdgcn_readfirstlane(k == 1) && mine) hc1 = a;
+        if (__builtin_amdgcn_readfirstlane(k == 2) && mine) hc2 = a;
+        if (__builtin_amdgcn_readfirstlane(k == 3) && mine) hc3 = a;
+      }
       if (j <= n + 1) arow[j] = A[(int64_t)a * p.ld + j];
-      if (col && hlen < R) hist[hlen * HL + j] = Bm[(int64_t)a * p.ld + j];
-      ++hlen;
+      const float bv_new = col ? Bm[(int64_t)a * p.ld + j] : 0.0f;
+      if (hl < RREG) hput(hl, bv_new);
+      else if (hl < RREG + LT && col) hist_j[hl - RREG] = bv_new;
+      ++hl;
     }
     __syncthreads();
   }
 
-  // Native order (Algorithm 1 step 4): kept positions are the set bits of the
-  // selection mask, counted in ascending index order.
+  // ---- native order (Algorithm 1 step 4): ascending positions of the set bits
   __syncthreads();
   int32_t* red32 = reinterpret_cast<int32_t*>(red);
   const uint64_t ballot = __ballot(j < n && selected);
@@ -354,9 +475,11 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
                          a.kept_idx, a.kept_cnt, a.err);
     return hipGetLastError();
   }
+  record_event(a.events, 0, stream);
   hipError_t e = launch_gram_gemm(a.dtype, a.KQV, a.T_vis, a.h, a.grp_off, a.G, a.max_group,
                                   a.gram, a.gram_group_stride, a.gram_ld, a.err, stream);
   if (e != hipSuccess) return e;
+  record_event(a.events, 1, stream);
 
   const int cols_per_block = 32;
   const dim3 ck_grid((a.max_group + 1 + cols_per_block - 1) / cols_per_block, a.G);
@@ -402,25 +525,43 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.err = a.err;
 
   const int threads = (a.max_group + 2 + 63) / 64 * 64;
-  p.hist_ld = (int)align_up((size_t)a.max_group + 1, 4);
-  const size_t fixed = (size_t)SelLds(0, p.hist_ld, a.max_cap).total;
-  const size_t row_bytes = (size_t)p.hist_ld * 4;
-  size_t rows = fixed < (size_t)kLdsBytes ? ((size_t)kLdsBytes - fixed) / row_bytes : 0;
-  const size_t want = (size_t)a.max_cap + 1;
-  if (rows > want) rows = want;
-  p.hist_lds_rows = (int)rows;
-  const size_t lds = (size_t)SelLds((int)rows, p.hist_ld, a.max_cap).total;
-
-  if (trace) {
-    hipFuncSetAttribute((const void*)select_kernel<true>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(select_kernel<true>, dim3(a.G), dim3(threads), lds, stream, p);
-  } else {
-    hipFuncSetAttribute((const void*)select_kernel<false>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(select_kernel<false>, dim3(a.G), dim3(threads), lds, stream, p);
+  const int nt_class = threads <= 320 ? 320 : threads <= 640 ? 640 : 1024;
+  const int need = a.max_cap + 1;                       // longest possible history
+  // History registers per thread: the VGPR budget is 512 / (waves per SIMD),
+  // so 16 waves allow 64 values, 10 waves 96 and 5 waves 128.
+  const int rmax = nt_class == 1024 ? 64 : nt_class == 640 ? 96 : 128;
+  int rreg = (need + 31) / 32 * 32;
+  if (rreg > rmax) rreg = rmax;
+  p.alpha_ld = (int)align_up((size_t)a.max_cap + 2, 16);
+  const size_t fixed = (size_t)SelLds(0, a.max_group, a.max_cap, p.alpha_ld).total;
+  const size_t per_entry = (size_t)(a.max_group + 1) * 4;   // one LDS history entry, all columns
+  size_t lt_max = fixed < (size_t)kLdsBytes ? ((size_t)kLdsBytes - fixed) / per_entry : 0;
+  // Column stride of 8k + 4 floats keeps the 16-byte reads of eight
+  // consecutive columns on distinct banks.
+  lt_max = lt_max >= 4 ? (lt_max - 4) / 8 * 8 + 4 : 0;
+  size_t lt = 0;
+  if (need > rreg) {
+    lt = (size_t)(need - rreg + 3) / 8 * 8 + 4;   // smallest 8k + 4 >= the entries needed
+    if (lt > lt_max) lt = lt_max;
   }
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  p.lds_tier = (int)lt;
+  const size_t lds = (size_t)SelLds((int)lt, a.max_group, a.max_cap, p.alpha_ld).total;
+
+  const void* fn = nullptr;
+#define SP_PICK(NT, RR)                                                             \
+  if (nt_class == NT && rreg == RR)                                                 \
+    fn = trace ? (const void*)select_kernel<NT, RR, true> : (const void*)select_kernel<NT, RR, false>;
+  SP_PICK(320, 32) SP_PICK(320, 64) SP_PICK(320, 96) SP_PICK(320, 128)
+  SP_PICK(640, 32) SP_PICK(640, 64) SP_PICK(640, 96)
+  SP_PICK(1024, 32) SP_PICK(1024, 64)
+#undef SP_PICK
+  if (!fn) return hipErrorInvalidValue;
+  record_event(a.events, 2, stream);
+  if ((e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) != hipSuccess)
+    return e;
+  void* kargs[] = {&p};
+  if ((e = hipLaunchKernel(fn, dim3(a.G), dim3(threads), kargs, lds, stream)) != hipSuccess) return e;
+  record_event(a.events, 3, stream);
 
   hipLaunchKernelGGL(finalize_kernel, dim3(a.B), dim3(256), 0, stream, a.img_off, a.B, a.grp_off,
                      a.grp_img, a.G, a.grp_kept, a.grp_count, a.max_cap, a.kept_off, a.kept_idx,

@@ -22,6 +22,11 @@ constexpr int kLdsBytes = 160 * 1024;  // LDS per workgroup on gfx950
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Records events[i] on the stream when the caller supplied it.
+inline void record_event(const hipEvent_t* events, int i, hipStream_t stream) {
+  if (events && events[i]) (void)hipEventRecord(events[i], stream);
+}
+
 __device__ inline void set_device_error(int32_t* err, int32_t code) {
   atomicCAS(err, 0, code);
 }
@@ -78,6 +83,7 @@ struct SelectArgs {
   int32_t* grp_kept;     // [G, max_cap]
   int32_t* grp_count;    // [G]
   int32_t* err;
+  const hipEvent_t* events;
 };
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 

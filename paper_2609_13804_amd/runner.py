@@ -99,14 +99,15 @@ class DeviceRun:
         self.ws = [torch.zeros(n, dtype=torch.uint8, device=dev) for n in self.ws_bytes]
 
     # ---------------------------------------------------------------- stages
-    def project(self, stream=None, g_text: float = 1.0, ln_eps: float = 1e-5):
+    def project(self, stream=None, g_text: float = 1.0, ln_eps: float = 1e-5, events=None):
         s = self.sizes
         return sp.stepprune_project(self.dims, self.X, s.T_vis, self.s_start, self.s_stop,
                                     self.W_kqv, self.E, self.text_off, s.B, s.T_txt, self.W_text,
                                     g_text, ln_eps, self.KQV, self.ctx, self.ws[0],
-                                    self.ws_bytes[0], stream)
+                                    self.ws_bytes[0], stream, events=events)
 
-    def select(self, stream=None, b_stop: Optional[float] = None, flags: Optional[int] = None):
+    def select(self, stream=None, b_stop: Optional[float] = None, flags: Optional[int] = None,
+               events=None):
         s = self.sizes
         return sp.stepprune_select(self.dims, self.KQV, self.ctx, s.T_vis, self.img_off, s.B,
                                    self.grp_off, self.grp_img, self.grp_cap, s.G, s.max_group,
@@ -114,14 +115,15 @@ class DeviceRun:
                                    self.b_stop if b_stop is None else b_stop, 1,
                                    self.flags if flags is None else flags, self.kept_idx,
                                    self.kept_cnt, self.grp_cnt, self.trace, self.trace_steps,
-                                   self.ws[1], self.ws_bytes[1], stream)
+                                   self.ws[1], self.ws_bytes[1], stream, events=events)
 
-    def compact(self, stream=None):
+    def compact(self, stream=None, events=None):
         s = self.sizes
         return sp.stepprune_compact(self.dims, self.X, self.img_off, self.E, self.text_off,
                                     self.kept_idx, self.kept_off, self.kept_cnt, s.B,
                                     self.layout_code, self.rows_per_image, self.out_rows, self.out,
-                                    self.seq_info, self.ws[2], self.ws_bytes[2], stream)
+                                    self.seq_info, self.ws[2], self.ws_bytes[2], stream,
+                                    events=events)
 
     def run(self, stream=None):
         self.project(stream)

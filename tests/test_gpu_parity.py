@@ -222,3 +222,25 @@ def test_device_error_on_oversized_group(gpu_lib):
     torch.cuda.synchronize()
     assert sp.stepprune_read_device_error(run.ws[1]) == sp.SP_DEV_GROUP_TOO_LARGE
     assert sp.stepprune_read_device_error(run.ws[1]) == 0     # read clears it
+
+
+def test_long_episodes_cross_every_history_tier(gpu_lib):
+    """Episodes far longer than the register-resident history: caps of 400 on
+    576-token groups with STOP disabled, so the history passes the register
+    slots, the LDS rows and the re-read tier; every step still matches the
+    oracle (staged, teacher-forced)."""
+    w0 = W.WORKLOADS["mid_bf16"]
+    lay0 = W.make_layout(w0)
+    caps = np.minimum(np.diff(lay0.grp_off), 400)
+    w, inp, lay, run = _setup("mid_bf16", b_stop=-math.inf, caps=caps)
+    run.run()
+    torch.cuda.synchronize()
+    _check_errors(run)
+    KQV, ctx = _staged(run)
+    actions = run.trace_actions()
+    assert [len(a) for a in actions] == [int(c) if c <= n else int(n) + 1
+                                         for c, n in zip(caps, np.diff(lay.grp_off))]
+    rep = parity.check_selection(KQV, ctx, lay.grp_off, lay.grp_img, caps, -math.inf, w.h,
+                                 actions, run.trace.cpu().numpy(), w.dtype)
+    print(f"long episodes: {rep.steps} steps, {rep.exempt_steps} exempt, "
+          f"max logit err {rep.max_logit_err:.2e}")
