@@ -178,6 +178,177 @@ __device__ __forceinline__ void gemm_block(const ARows& ar, const BRows& br, int
     }
 }
 
+// ------------------------------------------------------------------ bf16, 256 x 256 tiles
+//
+// Large bfloat16 GEMMs: a 256 x 256 output tile per workgroup of four waves
+// (each wave 128 x 128 = 4 x 4 MFMA 32x32x16 tiles, accumulators in AGPRs),
+// K in 32-wide stages.  Operand tiles go straight from global memory into LDS
+// (global_load_lds_dwordx4: one wave instruction fills 1 KiB = 16 rows x 64
+// bytes) through a ring of S stage buffers, loads running S - 1 stages ahead
+// of the matrix cores.  Within a 64-byte row the four 16-byte chunks are
+// stored XOR-swizzled (chunk c of row r at slot c ^ ((r >> 1) & 3)), which the
+// load realises by choosing each lane's source address, so that the 16-byte
+// fragment reads of consecutive rows hit distinct banks.  Rows past M (N) are
+// clamped to the last valid row and their results are not stored.
+constexpr int kBM = 256, kBN = 256, kBK = 32, kStages = 4;
+constexpr int kOpBytes = kBM * kBK * 2;                // one operand tile, 16 KiB
+constexpr int kStageBytes = 2 * kOpBytes;              // A and B, 32 KiB
+constexpr int kLoadsPerWave = 2 * kOpBytes / 1024 / 4; // DMA instructions per wave per stage
+
+typedef __attribute__((address_space(1))) const void* gptr_t;
+typedef __attribute__((address_space(3))) void* lptr_t;
+
+__device__ __forceinline__ void lds_dma16(const void* src, char* dst) {
+  __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)dst, 16, 0, 0);
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Byte offset of (row, 16-byte chunk) in a swizzled operand tile (64-byte rows).
+__device__ __forceinline__ int swz(int row, int chunk) {
+  return row * 64 + ((chunk ^ ((row >> 1) & 3)) << 4);
+}
+
+template <typename OutT, class ARows, class BRows>
+__device__ __forceinline__ void gemm_bf16_256(const ARows& ar, const BRows& br, int64_t M,
+                                              int64_t N, int K, OutT* __restrict__ C, int64_t ldc,
+                                              int64_t m0, int64_t n0, char* smem) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // This wave loads 16-row groups wave + 4 i (i < 4) of both operand tiles;
+  // lane (rl = lane / 4, slot = lane % 4) fetches chunk slot ^ ((rl >> 1) & 3)
+  // of row rl.
+  const int rl = lane >> 2;
+  const int chunk = (lane & 3) ^ ((rl >> 1) & 3);
+  const __bf16* pa[4];
+  const __bf16* pb[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = 16 * (wave + 4 * i) + rl;
+    const int64_t gm = m0 + r < M ? m0 + r : M - 1;
+    const int64_t gn = n0 + r < N ? n0 + r : N - 1;
+    pa[i] = ar.row(gm) + chunk * 8;
+    pb[i] = br.row(gn) + chunk * 8;
+  }
+  auto issue = [&](int buf, int k0) {
+    char* a = smem + buf * kStageBytes;
+    char* b = a + kOpBytes;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) lds_dma16(pa[i] + k0, a + (wave + 4 * i) * 1024);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) lds_dma16(pb[i] + k0, b + (wave + 4 * i) * 1024);
+  };
+
+  f32x16_t acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int arow0 = wm * 128 + (lane & 31);
+  const int brow0 = wn * 128 + (lane & 31);
+  const int khalf = lane >> 5;
+  auto load_frags = [&](const char* As, const char* Bs, int ks, bf16x8_t (&a)[4], bf16x8_t (&b)[4]) {
+    const int c = ks * 2 + khalf;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const bf16x8_t*>(As + swz(arow0 + 32 * i, c));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) b[j] = *reinterpret_cast<const bf16x8_t*>(Bs + swz(brow0 + 32 * j, c));
+  };
+
+  // Software pipeline over K stages.  Iteration kt multiplies stage kt in two
+  // halves (16 k each); between them it waits for stage kt + 1, passes the
+  // workgroup barrier, refills the ring with stage kt + S - 1 and starts
+  // reading stage kt + 1's fragments, so the barrier and the LDS latency hide
+  // behind matrix-core work.
+  const int KT = K / kBK;
+#pragma unroll
+  for (int s = 0; s < kStages - 1; ++s)
+    if (s < KT) issue(s, s * kBK);
+  if (KT > kStages - 2) wait_vmcnt<(kStages - 2) * kLoadsPerWave>();
+  else wait_vmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  bf16x8_t a0[4], b0[4], a1[4], b1[4];
+  load_frags(smem, smem + kOpBytes, 0, a0, b0);
+  load_frags(smem, smem + kOpBytes, 1, a1, b1);
+  for (int kt = 0; kt < KT; ++kt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[i], b0[j], acc[i][j], 0, 0, 0);
+    bf16x8_t na0[4], nb0[4], na1[4], nb1[4];
+    const bool more = kt + 1 < KT;
+    if (more) {
+      // Stage kt + 1 has landed once at most (stages issued after it) x loads
+      // of this wave remain; all fragment reads of stage kt are complete.
+      if (kt + kStages - 1 < KT) wait_vmcnt<(kStages - 3) * kLoadsPerWave>();
+      else wait_vmcnt<0>();
+      __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+      // Bare s_barrier (no fence): a workgroup fence would wait for every load
+      // still in flight and collapse the ring to a single stage.
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      if (kt + kStages - 1 < KT) issue((kt + kStages - 1) % kStages, (kt + kStages - 1) * kBK);
+      const char* As = smem + ((kt + 1) % kStages) * kStageBytes;
+      load_frags(As, As + kOpBytes, 0, na0, nb0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b1[j], acc[i][j], 0, 0, 0);
+    if (more) {
+      const char* As = smem + ((kt + 1) % kStages) * kStageBytes;
+      load_frags(As, As + kOpBytes, 1, na1, nb1);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a0[i] = na0[i];
+        b0[i] = nb0[i];
+        a1[i] = na1[i];
+        b1[i] = nb1[i];
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // 32x32 MFMA result layout: lane l, register r holds
+  // row 8*(r/4) + 4*(l/32) + r%4, column l%32.
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t col = n0 + wn * 128 + j * 32 + (lane & 31);
+      if (col >= N) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (row < M) C[row * ldc + col] = store_cvt<OutT>(acc[i][j][r]);
+      }
+    }
+}
+
+// Workgroup w runs on XCD w % 8; give each XCD a contiguous run of tiles (in
+// N-fastest order) so that tiles sharing an A panel run side by side and share
+// that XCD's L2.  Returns -1 for the padding workgroups of the last run.
+__device__ __forceinline__ int64_t xcd_tile(int64_t w, int64_t tiles) {
+  const int64_t per = (tiles + 7) / 8;
+  const int64_t t = (w % 8) * per + w / 8;
+  return t < tiles ? t : -1;
+}
+
 // ------------------------------------------------------------------ row maps
 
 template <typename T>
@@ -241,6 +412,18 @@ __global__ __launch_bounds__(kThreads) void project_gemm_kernel(ProjRows<T> ar, 
   gemm_block<T, OutT, BM, BN, BK>(ar, br, M, N, K, C, N, (t / nt) * BM, (t % nt) * BN, smem);
 }
 
+__global__ __launch_bounds__(kThreads) void project_gemm_bf16_kernel(ProjRows<__bf16> ar,
+                                                                    DenseRows<__bf16> br,
+                                                                    int64_t M, int64_t N, int K,
+                                                                    uint16_t* C) {
+  __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes];
+  const int64_t nt = (N + kBN - 1) / kBN;
+  const int64_t tiles = ((M + kBM - 1) / kBM) * nt;
+  const int64_t t = xcd_tile(blockIdx.x, tiles);
+  if (t < 0) return;
+  gemm_bf16_256<uint16_t>(ar, br, M, N, K, C, N, (t / nt) * kBM, (t % nt) * kBN, smem);
+}
+
 template <typename T, int BM, int BN, int BK>
 __global__ __launch_bounds__(kThreads) void dense_gemm_kernel(DenseRows<T> ar, DenseRows<T> br,
                                                               int64_t M, int64_t N, int K,
@@ -285,14 +468,11 @@ hipError_t launch_project_gemm(int dtype, const void* X, int64_t T_vis, const vo
                                hipStream_t stream) {
   const int64_t M = T_vis + 2, N = n_out;
   if (dtype == SP_BF16) {
-    constexpr int BM = 256, BN = 256, BK = 64;
-    using T = uint16_t;
     ProjRows<__bf16> ar{(const __bf16*)X, T_vis, (const __bf16*)s_start, (const __bf16*)s_stop, d};
     DenseRows<__bf16> br{(const __bf16*)W, d};
-    (void)sizeof(T);
-    hipLaunchKernelGGL((project_gemm_kernel<__bf16, uint16_t, BM, BN, BK>),
-                       dim3((unsigned)(ceil_div(M, BM) * ceil_div(N, BN))), dim3(kThreads), 0, stream,
-                       ar, br, M, N, d, (uint16_t*)out);
+    const int64_t tiles = ceil_div(M, kBM) * ceil_div(N, kBN);
+    hipLaunchKernelGGL(project_gemm_bf16_kernel, dim3((unsigned)(ceil_div(tiles, 8) * 8)),
+                       dim3(kThreads), 0, stream, ar, br, M, N, d, (uint16_t*)out);
   } else {
     constexpr int BM = 128, BN = 128, BK = 32;
     ProjRows<float> ar{(const float*)X, T_vis, (const float*)s_start, (const float*)s_stop, d};
