@@ -84,7 +84,9 @@ def _episode_steps(caps, sizes, kept):
 
 
 def cpu_baseline(w, lay, b_stop, budget_s):
-    """The oracle (float64 NumPy, as written) over a bounded sample of the batch."""
+    """The oracle (float64 NumPy, as written) over a bounded sample of the batch:
+    chunks of up to 4 images, passing over the batch again until the oracle has
+    run for the time budget."""
     import numpy as np
     import oracle
     from paper_2609_13804_amd import workloads as W
@@ -97,10 +99,12 @@ def cpu_baseline(w, lay, b_stop, budget_s):
     elapsed = 0.0
     chunk = max(1, min(4, w.batch))
     images = list(range(w.batch))
-    while done < w.batch and elapsed < budget_s:
-        sub = images[done:done + chunk]
-        inp = W.make_inputs(w, sub)
-        sl = W.make_layout(w, sub)
+    chunks = [images[i:i + chunk] for i in range(0, w.batch, chunk)]
+    k = 0
+    while elapsed < budget_s:
+        sub = chunks[k % len(chunks)]
+        k += 1
+        inp, sl = W.make_inputs(w, sub), W.make_layout(w, sub)     # not timed
         t0 = time.perf_counter()
         KQV = oracle.project(inp["X"], inp["s_start"], inp["s_stop"], inp["W_kqv"], w.dtype)
         ctx = oracle.text_context(inp["E_text"], sl.text_off, inp["W_text"])
@@ -112,8 +116,47 @@ def cpu_baseline(w, lay, b_stop, budget_s):
         elapsed += time.perf_counter() - t0
         done += len(sub)
     return {"value": done / elapsed, "unit": "images/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{done} of the {w.batch} images of the {w.name} batch, one pass of "
-                      f"project + select + compact in float64 ({elapsed:.1f} s)"}
+            "sample": f"{done} images ({done / w.batch:.2f} passes over the {w.batch}-image "
+                      f"{w.name} batch, chunks of {chunk}) of project + select + compact in "
+                      f"float64, {elapsed:.1f} s"}
+
+
+def copy_probe(mib):
+    """A plain device-to-device copy of a known size: under rocprofv3 --pmc its
+    FETCH_SIZE and WRITE_SIZE readings calibrate the same counters taken on the
+    library's kernels (bytes counted per byte moved)."""
+    import torch
+    n = mib << 20
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").random_(0, 255)
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n, "launches": 5}), flush=True)
+    return 0
+
+
+def hbm_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter summary,
+    or None when there is none or the kernel's source has changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{kernel}_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    for line in open(path):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.split("=", 1)
+            rec[k.strip()] = v.strip()
+    digest = hashlib.sha256()
+    for name in rec.get("source", "").split():
+        src = os.path.join(ROOT, "paper_2609_13804_amd", "csrc", name)
+        if not os.path.isfile(src):
+            return None
+        digest.update(open(src, "rb").read())
+    if not rec.get("source") or digest.hexdigest() != rec.get("source_sha256"):
+        return None
+    return float(rec["bytes_per_launch"])
 
 
 def main(argv=None):
@@ -123,9 +166,14 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llava15_bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=20.0,
+    ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle work for the CPU baseline sample")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run a plain device copy of this many MiB (5 launches), the "
+                         "calibration for the FETCH_SIZE / WRITE_SIZE counters, and exit")
     args = ap.parse_args(argv)
+    if args.copy_probe_mib:
+        return copy_probe(args.copy_probe_mib)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU only: the selection path shards by image with no "
@@ -212,7 +260,8 @@ def main(argv=None):
     bound, amount, peak, unit = work[dom]
     achieved = amount / (kernels[dom] * 1e-6)
     roofline = {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": unit,
-                "frac": round(achieved / peak, 4), "traffic": None, "kernel": dom,
+                "frac": round(achieved / peak, 4), "traffic": hbm_traffic(dom, w.name),
+                "kernel": dom,
                 "algorithmic": f"{amount:.6g} {'TFLOP' if unit == 'TFLOP/s' else 'GB'} per launch"}
 
     elapsed = t1 - t0
