@@ -1,0 +1,147 @@
+"""The five paper-shaped batches at full size, launched exactly as bench.py
+launches them (one stream, untraced selection kernel), checked against the
+oracle on outputs it can compute one by one:
+
+  * projection: a seeded sample of rows plus the START and STOP rows;
+  * text context: a sample of images;
+  * selection: every episode's count and kept set against the traced kernel's
+    own action sequence (which must take the same decisions as the untraced
+    kernel), and a sample of episodes (always including the longest and a
+    capped one) replayed teacher-forced and free-running in the oracle on the
+    GPU's projected rows (tests/parity.py protocol);
+  * compaction: three feature columns of every output row for the whole batch,
+    and every column of the rows of a sample of images, bit-exact.
+
+Tolerances are those of tests/parity.py.
+"""
+import gc
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_13804_amd import binding as sp
+from paper_2609_13804_amd import workloads as W
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+
+SAMPLE_ROWS = 384
+SAMPLE_GROUPS = 16
+SAMPLE_IMAGES = 3
+
+
+def _sample_groups(rng, sizes, caps, steps, k):
+    """k groups: the longest episode, a capped one if any, the rest at random."""
+    G = len(sizes)
+    chosen = [int(np.argmax(steps))]
+    capped = [g for g in range(G) if steps[g] == min(int(caps[g]), int(sizes[g])) and caps[g] > 0]
+    if capped:
+        chosen.append(int(capped[len(capped) // 2]))
+    rest = [g for g in range(G) if g not in chosen]
+    extra = rng.choice(rest, size=min(len(rest), max(0, k - len(chosen))), replace=False)
+    return sorted(set(chosen) | set(int(g) for g in extra))
+
+
+def _sub_episodes(KQV_dev, grp_off, groups, T_vis):
+    """Host float64 copy of the sampled groups' rows followed by the START and
+    STOP rows, with the group offsets into it."""
+    rows = np.concatenate([np.arange(grp_off[g], grp_off[g + 1]) for g in groups]
+                          + [np.array([T_vis, T_vis + 1])])
+    sub = KQV_dev[torch.from_numpy(rows).to(KQV_dev.device)].double().cpu().numpy()
+    sizes = [int(grp_off[g + 1] - grp_off[g]) for g in groups]
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    return sub, off
+
+
+@pytest.mark.parametrize("name", W.PAPER_WORKLOADS)
+def test_full_size_parity(gpu_lib, name):
+    from paper_2609_13804_amd.runner import DeviceRun
+    w = W.WORKLOADS[name]
+    lay = W.make_layout(w)
+    inp = W.make_inputs(w)
+    b_stop = W.stop_bias(w)
+    sizes = np.diff(lay.grp_off)
+    steps_max = int(max(min(int(c), int(n)) for c, n in zip(lay.grp_cap, sizes))) + 1
+    print(f"{name}: {lay.batch} images, {lay.groups} groups, {int(lay.img_off[-1])} tokens",
+          flush=True)
+    run = DeviceRun(w, inp, lay, b_stop, trace_steps=steps_max)
+    rng = np.random.default_rng([2609, w.cfg_id])
+
+    # ---- the benchmark's launch sequence
+    run.project()
+    run.select(flags=0)
+    if run.out is not None:
+        run.compact()
+    torch.cuda.synchronize()
+    assert run.device_errors() == [0, 0, 0]
+    kept = run.kept_lists()
+    grp_cnt = run.grp_cnt.cpu().numpy()[:lay.groups]
+    T_vis = int(lay.img_off[-1])
+
+    # ---- projection, sampled rows
+    rows = np.sort(rng.choice(T_vis, size=min(SAMPLE_ROWS, T_vis), replace=False))
+    want = oracle.project(inp["X"][rows], inp["s_start"], inp["s_stop"], inp["W_kqv"], w.dtype)
+    idx = torch.from_numpy(np.concatenate([rows, [T_vis, T_vis + 1]])).to(run.KQV.device)
+    got = run.KQV[idx].double().cpu().numpy()
+    tol = parity.logit_tol(w.dtype)
+    assert parity.rows_relerr(got, want) <= tol
+    if w.dtype == "bf16":
+        assert np.count_nonzero(got != want) / got.size <= 1e-2
+
+    # ---- text context, sampled images
+    imgs = sorted({0, lay.batch - 1} | set(int(b) for b in rng.choice(lay.batch, SAMPLE_IMAGES)))
+    ctx = run.ctx.double().cpu().numpy()
+    for b in imgs:
+        t0, t1 = int(lay.text_off[b]), int(lay.text_off[b + 1])
+        c = oracle.text_context(inp["E_text"][t0:t1], np.array([0, t1 - t0]), inp["W_text"])
+        assert parity.rows_relerr(ctx[b:b + 1], c) <= 1e-5, f"image {b}"
+
+    # ---- selection: the traced kernel decides as the benchmarked one did
+    run.select(flags=sp.SP_TRACE)
+    torch.cuda.synchronize()
+    assert run.device_errors() == [0, 0, 0]
+    actions = run.trace_actions()
+    assert run.kept_lists() == kept
+    assert kept == parity.kept_from_actions(actions, lay.grp_off, lay.grp_img, lay.img_off,
+                                            lay.batch)
+    assert grp_cnt.tolist() == [sum(1 for a in s if a != -1) for s in actions]
+    for g, s in enumerate(actions):
+        cap = min(int(lay.grp_cap[g]), int(sizes[g]))
+        assert (s and s[-1] == -1 and len(s) <= cap + 1) or len(s) == int(lay.grp_cap[g]), g
+    steps = np.array([len(s) for s in actions])
+
+    groups = _sample_groups(rng, sizes, lay.grp_cap, steps, SAMPLE_GROUPS)
+    sub, sub_off = _sub_episodes(run.KQV, lay.grp_off, groups, T_vis)
+    trace = run.trace.cpu().numpy()[groups]
+    rep = parity.check_selection(sub, ctx, sub_off, lay.grp_img[groups], lay.grp_cap[groups],
+                                 b_stop, w.h, [actions[g] for g in groups], trace, w.dtype)
+    print(f"{name}: checked {rep.episodes} of {lay.groups} episodes ({rep.steps} steps, longest "
+          f"{int(steps.max())}), {rep.exempt_steps} exempt, max logit err "
+          f"{rep.max_logit_err:.2e}, free-running equal {rep.free_running_equal}/"
+          f"{rep.free_running_checked}; kept total {sum(map(len, kept))}", flush=True)
+    del sub
+
+    # ---- compaction
+    if run.out is not None:
+        cols = [0, w.d // 2, w.d - 1]
+        out_cols = run.out[:, cols].float().cpu().numpy()
+        want_cols, seq = oracle.compact(inp["X"][:, cols], lay.img_off, inp["E_text"][:, cols],
+                                        lay.text_off, kept, w.layout, lay.rows_per_image,
+                                        np.zeros((run.out_rows, len(cols))))
+        assert np.array_equal(out_cols, want_cols.astype(np.float32))
+        assert run.seq_info.cpu().numpy().tolist() == seq.tolist()
+        for b in imgs:
+            i0, i1 = int(lay.img_off[b]), int(lay.img_off[b + 1])
+            t0, t1 = int(lay.text_off[b]), int(lay.text_off[b + 1])
+            n_rows = len(kept[b]) + t1 - t0
+            base = b * lay.rows_per_image if w.layout == "padded" else int(seq[b])
+            got_rows = run.out[base:base + n_rows].float().cpu().numpy()
+            want_rows, _ = oracle.compact(inp["X"][i0:i1], np.array([0, i1 - i0]),
+                                          inp["E_text"][t0:t1], np.array([0, t1 - t0]), [kept[b]],
+                                          "packed", 0, np.zeros((n_rows, w.d)))
+            assert np.array_equal(got_rows, want_rows.astype(np.float32)), f"image {b}"
+    del run, inp
+    gc.collect()
+    torch.cuda.empty_cache()
