@@ -27,8 +27,12 @@
  *    on the same stream.
  *  - Errors that depend on device-resident data (inconsistent offsets, a group
  *    larger than the stated maximum, counts that do not fit the output) are
- *    recorded in a device error word inside `ws`; the affected outputs are
- *    then undefined.  stepprune_read_device_error() reads it.
+ *    recorded in a device error word, the first 4 bytes of `ws`; the affected
+ *    outputs are then undefined.  The word keeps the first error recorded
+ *    until stepprune_read_device_error() reads and clears it, so it covers
+ *    every call made with that workspace since the last read.  A new
+ *    workspace must be zero-filled (its first 256 bytes at least) before its
+ *    first use.
  *  - No C++ exception crosses this interface.
  *  - `events` (host) is NULL or points to caller-created hipEvent_t handles that
  *    the call records on `stream` around its main kernels, for timing:

@@ -23,21 +23,22 @@ sp_status check_dims(const sp_dims* d) {
 int elem_bytes(const sp_dims* d) { return d->dtype == SP_F32 ? 4 : 2; }
 
 struct SelectWs {
-  size_t gram, ck, kept, count, total;
+  size_t gram, csplit, kept, count, total;
   int64_t gstride;
-  int gram_ld, ck_ld;
+  int gram_ld;
 };
 
-SelectWs select_ws_layout(int G, int max_group, int max_cap) {
+// Header; Gram blocks [G][2 (max_group + 1) + 3][ld] float32; context split
+// [B][3][h] in the working dtype; group-local kept lists; group counts.
+SelectWs select_ws_layout(const sp_dims* d, int B, int G, int max_group, int max_cap) {
   SelectWs w;
   w.gram_ld = (int)align_up((size_t)max_group + 2, 4);
-  w.ck_ld = (int)align_up((size_t)max_group + 1, 4);
-  w.gstride = (int64_t)2 * (max_group + 1) * w.gram_ld;
+  w.gstride = (int64_t)(2 * (max_group + 1) + kGramExtraRows) * w.gram_ld;
   size_t off = kWsHeaderBytes;
   w.gram = off;
   off = align_up(off + (size_t)G * w.gstride * 4, 256);
-  w.ck = off;
-  off = align_up(off + (size_t)G * w.ck_ld * 4, 256);
+  w.csplit = off;
+  off = align_up(off + (size_t)B * kGramExtraRows * d->h * elem_bytes(d), 256);
   w.kept = off;
   off = align_up(off + (size_t)G * (max_cap > 0 ? max_cap : 1) * 4, 256);
   w.count = off;
@@ -46,8 +47,10 @@ SelectWs select_ws_layout(int G, int max_group, int max_cap) {
   return w;
 }
 
+// Header, then the text projection's K-split partial products [split][T_txt][h].
 size_t project_ws_bytes(const sp_dims* d, int64_t T_txt) {
-  return kWsHeaderBytes + align_up((size_t)T_txt * d->h * 4, 256);
+  const size_t split = (size_t)text_split(T_txt, d->h, d->d_text);
+  return kWsHeaderBytes + align_up(split * (size_t)T_txt * d->h * 4, 256);
 }
 
 sp_status hip_status(hipError_t e) { return e == hipSuccess ? SP_OK : SP_EHIP; }
@@ -75,7 +78,7 @@ size_t stepprune_workspace_bytes(int32_t which, const sp_dims* dims, int64_t T_v
     case 0: return project_ws_bytes(dims, T_txt);
     case 1:
       if (max_group < 0 || max_group > kMaxGroup || max_cap < 0) return 0;
-      return select_ws_layout(G, max_group, max_cap).total;
+      return select_ws_layout(dims, B, G, max_group, max_cap).total;
     case 2: return kWsHeaderBytes;
   }
   return 0;
@@ -100,16 +103,15 @@ sp_status stepprune_project(const sp_dims* dims, const void* X, int64_t T_vis, c
 
   int32_t* err = reinterpret_cast<int32_t*>(ws);
   float* tproj = reinterpret_cast<float*>(static_cast<char*>(ws) + kWsHeaderBytes);
-  hipError_t e = launch_clear_error(err, stream);
   record_event(events, 0, stream);
-  if (e == hipSuccess)
-    e = launch_project_gemm(dims->dtype, X, T_vis, s_start, s_stop, W_kqv, dims->d, 3 * dims->h,
-                            KQV, stream);
+  hipError_t e = launch_project_gemm(dims->dtype, X, T_vis, s_start, s_stop, W_kqv, dims->d,
+                                     3 * dims->h, KQV, stream);
   record_event(events, 1, stream);
   if (e == hipSuccess)
     e = launch_text_gemm(dims->dtype, E_text, T_txt, W_text, dims->d_text, dims->h, tproj, stream);
   if (e == hipSuccess)
-    e = launch_text_pool(tproj, text_off, B, T_txt, dims->h, g_text, ln_eps, ctx, err, stream);
+    e = launch_text_pool(tproj, text_split(T_txt, dims->h, dims->d_text), text_off, B, T_txt,
+                         dims->h, g_text, ln_eps, ctx, err, stream);
   return hip_status(e);
 }
 
@@ -134,7 +136,7 @@ sp_status stepprune_select(const sp_dims* dims, const void* KQV, const float* ct
   if ((flags & SP_TRACE) && trace_steps > 0 && !trace) return SP_EINVAL;
   if (b_stop != b_stop) return SP_EINVAL;   // NaN
   if (!aligned16(KQV) || !aligned16(ctx) || !aligned16(ws)) return SP_EINVAL;
-  const SelectWs lay = select_ws_layout(G, max_group, max_cap);
+  const SelectWs lay = select_ws_layout(dims, B, G, max_group, max_cap);
   if (ws_bytes < lay.total) return SP_EWORKSPACE;
 
   char* wsb = static_cast<char*>(ws);
@@ -163,15 +165,12 @@ sp_status stepprune_select(const sp_dims* dims, const void* KQV, const float* ct
   a.gram = reinterpret_cast<float*>(wsb + lay.gram);
   a.gram_group_stride = lay.gstride;
   a.gram_ld = lay.gram_ld;
-  a.cK = reinterpret_cast<float*>(wsb + lay.ck);
-  a.ck_ld = lay.ck_ld;
+  a.csplit = wsb + lay.csplit;
   a.grp_kept = reinterpret_cast<int32_t*>(wsb + lay.kept);
   a.grp_count = reinterpret_cast<int32_t*>(wsb + lay.count);
   a.err = reinterpret_cast<int32_t*>(wsb);
   a.events = events;
-  hipError_t e = launch_clear_error(a.err, stream);
-  if (e == hipSuccess) e = launch_select(a, stream);
-  return hip_status(e);
+  return hip_status(launch_select(a, stream));
 }
 
 sp_status stepprune_compact(const sp_dims* dims, const void* X, const int32_t* img_off,
@@ -209,9 +208,8 @@ sp_status stepprune_compact(const sp_dims* dims, const void* X, const int32_t* i
   a.out = out;
   a.seq_info = seq_info;
   a.err = reinterpret_cast<int32_t*>(ws);
-  hipError_t e = launch_clear_error(a.err, stream);
   record_event(events, 0, stream);
-  if (e == hipSuccess) e = launch_compact(a, stream);
+  hipError_t e = launch_compact(a, stream);
   record_event(events, 1, stream);
   return hip_status(e);
 }

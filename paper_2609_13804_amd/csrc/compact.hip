@@ -80,8 +80,6 @@ __global__ __launch_bounds__(kCompactWaves * 64) void compact_kernel(CompactArgs
   }
 }
 
-__global__ void clear_error_kernel(int32_t* err) { *err = 0; }
-
 }  // namespace
 
 hipError_t launch_compact(const CompactArgs& a, hipStream_t stream) {
@@ -92,11 +90,6 @@ hipError_t launch_compact(const CompactArgs& a, hipStream_t stream) {
   if (y > 256) y = 256;
   hipLaunchKernelGGL(compact_kernel, dim3((unsigned)y, (unsigned)a.B), dim3(kCompactWaves * 64), 0,
                      stream, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_clear_error(int32_t* err, hipStream_t stream) {
-  hipLaunchKernelGGL(clear_error_kernel, dim3(1), dim3(1), 0, stream, err);
   return hipGetLastError();
 }
 

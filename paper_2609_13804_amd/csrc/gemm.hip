@@ -372,18 +372,21 @@ struct DenseRows {
 };
 
 // Gram operand rows of one group with tokens [g0, g0 + n): A side is
-// [Q tokens; q_start; V tokens; v_start], B side is [K tokens; k_stop; k_start].
+// [Q tokens; q_start; V tokens; v_start; c_hi; c_mid; c_lo] (the last three
+// from the image's context split), B side is [K tokens; k_stop; k_start].
 template <typename T>
 struct GramARows {
   const T* KQV;
   int64_t g0, n, start_row;
   int h;
+  const T* csplit;     // the image's three context rows
   __device__ const T* row(int64_t r) const {
     const int64_t ld = 3 * (int64_t)h;
     if (r < n) return KQV + (g0 + r) * ld + h;
     if (r == n) return KQV + start_row * ld + h;
     if (r < 2 * n + 1) return KQV + (g0 + r - n - 1) * ld + 2 * h;
-    return KQV + start_row * ld + 2 * h;
+    if (r == 2 * n + 1) return KQV + start_row * ld + 2 * h;
+    return csplit + (r - 2 * n - 2) * h;
   }
 };
 
@@ -424,6 +427,8 @@ __global__ __launch_bounds__(kThreads) void project_gemm_bf16_kernel(ProjRows<__
   gemm_bf16_256<uint16_t>(ar, br, M, N, K, C, N, (t / nt) * kBM, (t % nt) * kBN, smem);
 }
 
+// grid.x: output tiles, grid.y: K split p, which covers k in [p K, (p + 1) K)
+// and writes partial product p at C + p M N.
 template <typename T, int BM, int BN, int BK>
 __global__ __launch_bounds__(kThreads) void dense_gemm_kernel(DenseRows<T> ar, DenseRows<T> br,
                                                               int64_t M, int64_t N, int K,
@@ -431,32 +436,110 @@ __global__ __launch_bounds__(kThreads) void dense_gemm_kernel(DenseRows<T> ar, D
   __shared__ __attribute__((aligned(16))) char smem[Tile<T, BM, BN, BK>::LDS_BYTES];
   const int64_t nt = (N + BN - 1) / BN;
   const int64_t t = blockIdx.x;
-  gemm_block<T, float, BM, BN, BK>(ar, br, M, N, K, C, N, (t / nt) * BM, (t % nt) * BN, smem);
+  const int64_t k0 = (int64_t)blockIdx.y * K;
+  DenseRows<T> a{ar.base + k0, ar.ld}, b{br.base + k0, br.ld};
+  gemm_block<T, float, BM, BN, BK>(a, b, M, N, K, C + blockIdx.y * M * N, N, (t / nt) * BM,
+                                   (t % nt) * BN, smem);
 }
 
-// grid.x: tiles of the largest group, grid.y: group.
-template <typename T, int BM, int BN, int BK>
-__global__ __launch_bounds__(kThreads) void gram_gemm_kernel(const T* KQV, int64_t T_vis, int h,
-                                                             const int32_t* grp_off, int max_group,
-                                                             float* gram, int64_t gstride, int ld,
-                                                             int32_t* err) {
-  __shared__ __attribute__((aligned(16))) char smem[Tile<T, BM, BN, BK>::LDS_BYTES];
-  const int g = blockIdx.y;
-  const int64_t g0 = grp_off[g], g1 = grp_off[g + 1];
-  const int64_t n = g1 - g0;
-  if (g0 < 0 || g1 > T_vis || n < 0 || n > max_group) {
-    if (blockIdx.x == 0 && threadIdx.x == 0)
-      set_device_error(err, n > max_group ? SP_DEV_GROUP_TOO_LARGE : SP_DEV_BAD_OFFSETS);
-    return;
+// The context of image b as three rows of the working dtype whose sum is the
+// float32 value exactly (bfloat16: successive round-to-nearest-even residuals,
+// 3 x 8 significant bits; float32: the value and two zero rows).
+template <typename T>
+__global__ __launch_bounds__(256) void ctx_split_kernel(const float* __restrict__ ctx, int h,
+                                                        T* __restrict__ csplit) {
+  const int b = blockIdx.x;
+  for (int i = threadIdx.x; i < h; i += blockDim.x) {
+    const float c = ctx[(int64_t)b * h + i];
+    T* out = csplit + (int64_t)b * kGramExtraRows * h + i;
+    if constexpr (sizeof(T) == 2) {
+      const uint16_t hi = f32_to_bf16_rne(c);
+      const float r1 = c - __uint_as_float((uint32_t)hi << 16);
+      const uint16_t mid = f32_to_bf16_rne(r1);
+      const float r2 = r1 - __uint_as_float((uint32_t)mid << 16);
+      const uint16_t lo = f32_to_bf16_rne(r2);
+      reinterpret_cast<uint16_t*>(out)[0] = hi;
+      reinterpret_cast<uint16_t*>(out)[h] = mid;
+      reinterpret_cast<uint16_t*>(out)[2 * h] = lo;
+    } else {
+      out[0] = c;
+      out[h] = 0.0f;
+      out[2 * h] = 0.0f;
+    }
   }
-  const int64_t M = 2 * (n + 1), N = n + 2;
-  const int64_t nt = (N + BN - 1) / BN;
-  const int64_t t = blockIdx.x;
+}
+
+// Workgroup w runs on XCD w % 8.  With at least eight groups, all tiles of a
+// group are placed on one XCD (group x + 8 k on XCD x) so that the group's
+// rows are fetched into one L2.
+__device__ __forceinline__ bool gram_tile(int64_t w, int per_group, int G, int xcd_grouped,
+                                          int64_t& g, int64_t& t) {
+  if (xcd_grouped) {
+    const int64_t i = w / 8;
+    g = w % 8 + 8 * (i / per_group);
+    t = i % per_group;
+  } else {
+    g = w / per_group;
+    t = w % per_group;
+  }
+  return g < G;
+}
+
+// Validates group g; on inconsistent offsets one workgroup records the error.
+__device__ __forceinline__ bool gram_group_ok(const GramArgs& a, int64_t g, int64_t t, int64_t& g0,
+                                              int64_t& n, int& b) {
+  g0 = a.grp_off[g];
+  const int64_t g1 = a.grp_off[g + 1];
+  n = g1 - g0;
+  b = a.grp_img[g];
+  if (g0 < 0 || g1 > a.T_vis || n < 0 || n > a.max_group || b < 0 || b >= a.B) {
+    if (t == 0 && threadIdx.x == 0)
+      set_device_error(a.err, n > a.max_group ? SP_DEV_GROUP_TOO_LARGE : SP_DEV_BAD_OFFSETS);
+    return false;
+  }
+  return true;
+}
+
+// bfloat16 Gram products on the 256 x 256 direct-to-LDS core: 15 tiles per
+// 576-token group, one round for 16 groups.
+__global__ __launch_bounds__(kThreads) void gram_gemm_bf16_kernel(GramArgs a, int per_group,
+                                                                 int xcd_grouped) {
+  __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes];
+  int64_t g, t, g0, n;
+  int b;
+  if (!gram_tile(blockIdx.x, per_group, a.G, xcd_grouped, g, t)) return;
+  if (!gram_group_ok(a, g, t, g0, n, b)) return;
+  const __bf16* KQV = static_cast<const __bf16*>(a.KQV);
+  const __bf16* cs = static_cast<const __bf16*>(a.csplit) + (int64_t)b * kGramExtraRows * a.h;
+  const int64_t M = 2 * (n + 1) + kGramExtraRows, N = n + 2;
+  const int64_t nt = (a.max_group + 2 + kBN - 1) / kBN;
+  const int64_t m0 = (t / nt) * kBM, n0 = (t % nt) * kBN;
+  if (m0 >= M || n0 >= N) return;   // tile outside this (smaller) group
+  GramARows<__bf16> ar{KQV, g0, n, a.T_vis, a.h, cs};
+  GramBRows<__bf16> br{KQV, g0, n, a.T_vis, a.h};
+  gemm_bf16_256<float>(ar, br, M, N, a.h, a.gram + g * a.gram_group_stride, a.gram_ld, m0, n0,
+                       smem);
+}
+
+// float32 Gram products on the 128 x 128 register-staged core.
+__global__ __launch_bounds__(kThreads) void gram_gemm_f32_kernel(GramArgs a, int per_group,
+                                                                int xcd_grouped) {
+  constexpr int BM = 128, BN = 128, BK = 32;
+  __shared__ __attribute__((aligned(16))) char smem[Tile<float, BM, BN, BK>::LDS_BYTES];
+  int64_t g, t, g0, n;
+  int b;
+  if (!gram_tile(blockIdx.x, per_group, a.G, xcd_grouped, g, t)) return;
+  if (!gram_group_ok(a, g, t, g0, n, b)) return;
+  const float* KQV = static_cast<const float*>(a.KQV);
+  const float* cs = static_cast<const float*>(a.csplit) + (int64_t)b * kGramExtraRows * a.h;
+  const int64_t M = 2 * (n + 1) + kGramExtraRows, N = n + 2;
+  const int64_t nt = (a.max_group + 2 + BN - 1) / BN;
   const int64_t m0 = (t / nt) * BM, n0 = (t % nt) * BN;
-  if (m0 >= M) return;   // whole block idle for this (smaller) group
-  GramARows<T> ar{KQV, g0, n, T_vis, h};
-  GramBRows<T> br{KQV, g0, n, T_vis, h};
-  gemm_block<T, float, BM, BN, BK>(ar, br, M, N, h, gram + g * gstride, ld, m0, n0, smem);
+  if (m0 >= M || n0 >= N) return;
+  GramARows<float> ar{KQV, g0, n, a.T_vis, a.h, cs};
+  GramBRows<float> br{KQV, g0, n, a.T_vis, a.h};
+  gemm_block<float, float, BM, BN, BK>(ar, br, M, N, a.h, a.gram + g * a.gram_group_stride,
+                                       a.gram_ld, m0, n0, smem);
 }
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -484,45 +567,55 @@ hipError_t launch_project_gemm(int dtype, const void* X, int64_t T_vis, const vo
   return hipGetLastError();
 }
 
+int text_split(int64_t T_txt, int h, int d_text) {
+  // Enough workgroups to cover the chip: split K while the tiles are fewer
+  // than 512, up to 8 ways, keeping each part a whole number of 64-wide stages.
+  const int64_t tiles = ceil_div(T_txt, 128) * ceil_div(h, 128);
+  int s = 1;
+  while (s < 8 && tiles * s < 512 && d_text % (2 * s * 64) == 0) s *= 2;
+  return s;
+}
+
 hipError_t launch_text_gemm(int dtype, const void* E, int64_t T_txt, const void* W, int d_text,
                             int h, float* out, hipStream_t stream) {
   if (T_txt == 0) return hipSuccess;
+  const int split = text_split(T_txt, h, d_text);
+  const int kpart = d_text / split;
+  const dim3 grid((unsigned)(ceil_div(T_txt, 128) * ceil_div(h, 128)), (unsigned)split);
   if (dtype == SP_BF16) {
-    constexpr int BM = 128, BN = 128, BK = 64;
     DenseRows<__bf16> ar{(const __bf16*)E, d_text};
     DenseRows<__bf16> br{(const __bf16*)W, d_text};
-    hipLaunchKernelGGL((dense_gemm_kernel<__bf16, BM, BN, BK>),
-                       dim3((unsigned)(ceil_div(T_txt, BM) * ceil_div(h, BN))), dim3(kThreads), 0,
-                       stream, ar, br, T_txt, (int64_t)h, d_text, out);
+    hipLaunchKernelGGL((dense_gemm_kernel<__bf16, 128, 128, 64>), grid, dim3(kThreads), 0, stream,
+                       ar, br, T_txt, (int64_t)h, kpart, out);
   } else {
-    constexpr int BM = 128, BN = 128, BK = 32;
     DenseRows<float> ar{(const float*)E, d_text};
     DenseRows<float> br{(const float*)W, d_text};
-    hipLaunchKernelGGL((dense_gemm_kernel<float, BM, BN, BK>),
-                       dim3((unsigned)(ceil_div(T_txt, BM) * ceil_div(h, BN))), dim3(kThreads), 0,
-                       stream, ar, br, T_txt, (int64_t)h, d_text, out);
+    hipLaunchKernelGGL((dense_gemm_kernel<float, 128, 128, 32>), grid, dim3(kThreads), 0, stream,
+                       ar, br, T_txt, (int64_t)h, kpart, out);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_gram_gemm(int dtype, const void* KQV, int64_t T_vis, int h,
-                            const int32_t* grp_off, int G, int max_group, float* gram,
-                            int64_t gram_group_stride, int gram_ld, int32_t* err,
-                            hipStream_t stream) {
-  if (G == 0) return hipSuccess;
-  const int64_t M = 2 * ((int64_t)max_group + 1), N = max_group + 2;
-  if (dtype == SP_BF16) {
-    constexpr int BM = 128, BN = 128, BK = 64;
-    hipLaunchKernelGGL((gram_gemm_kernel<__bf16, BM, BN, BK>),
-                       dim3((unsigned)(ceil_div(M, BM) * ceil_div(N, BN)), (unsigned)G),
-                       dim3(kThreads), 0, stream, (const __bf16*)KQV, T_vis, h, grp_off, max_group,
-                       gram, gram_group_stride, gram_ld, err);
+hipError_t launch_gram_gemm(const GramArgs& a, hipStream_t stream) {
+  if (a.G == 0) return hipSuccess;
+  const int64_t M = 2 * ((int64_t)a.max_group + 1) + kGramExtraRows, N = a.max_group + 2;
+  const int xcd_grouped = a.G >= 8;
+  if (a.dtype == SP_BF16) {
+    hipLaunchKernelGGL(ctx_split_kernel<__bf16>, dim3(a.B), dim3(256), 0, stream, a.ctx, a.h,
+                       (__bf16*)a.csplit);
+    const int per_group = (int)(ceil_div(M, kBM) * ceil_div(N, kBN));
+    const int64_t blocks =
+        xcd_grouped ? 8 * ceil_div(a.G, 8) * per_group : (int64_t)a.G * per_group;
+    hipLaunchKernelGGL(gram_gemm_bf16_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, a,
+                       per_group, xcd_grouped);
   } else {
-    constexpr int BM = 128, BN = 128, BK = 32;
-    hipLaunchKernelGGL((gram_gemm_kernel<float, BM, BN, BK>),
-                       dim3((unsigned)(ceil_div(M, BM) * ceil_div(N, BN)), (unsigned)G),
-                       dim3(kThreads), 0, stream, (const float*)KQV, T_vis, h, grp_off, max_group,
-                       gram, gram_group_stride, gram_ld, err);
+    hipLaunchKernelGGL(ctx_split_kernel<float>, dim3(a.B), dim3(256), 0, stream, a.ctx, a.h,
+                       (float*)a.csplit);
+    const int per_group = (int)(ceil_div(M, 128) * ceil_div(N, 128));
+    const int64_t blocks =
+        xcd_grouped ? 8 * ceil_div(a.G, 8) * per_group : (int64_t)a.G * per_group;
+    hipLaunchKernelGGL(gram_gemm_f32_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, a,
+                       per_group, xcd_grouped);
   }
   return hipGetLastError();
 }

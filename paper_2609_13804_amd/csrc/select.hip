@@ -8,7 +8,7 @@
 // By linearity l_t(j) = sigma (cK[j] + A[e, j] + sum_tau alpha_tau B[tau, j]) with
 //     A = [Q; q_start] [K; k_stop; k_start]^T,  B = [V; v_start] [K; k_stop]^T,
 //     cK = c [K; k_stop]^T,
-// and the history scores are sigma A[e, col(tau)].  A and B are dense
+// and the history scores are sigma A[e, col(tau)].  A, B and cK are dense
 // contractions computed once per group on the matrix cores (gemm.hip), so a
 // step needs only the rows A[e, :] and B[e, :] of the newest history entry e:
 // one dependent load, then O(t * n) float32 FMAs.  One workgroup runs one
@@ -19,7 +19,9 @@
 //
 // Gram layout per group (float32, row stride ld): rows [0, n) A rows of the
 // tokens, row n the A row of START, rows [n+1, 2n+1) B rows of the tokens,
-// row 2n+1 the B row of START; columns [0, n) tokens, n STOP, n+1 START.
+// row 2n+1 the B row of START, rows 2n+2 .. 2n+4 three parts of cK whose sum
+// is cK (the context enters the products as three rows of the working dtype);
+// columns [0, n) tokens, n STOP, n+1 START.
 #include "sp_internal.h"
 
 namespace sp {
@@ -27,91 +29,14 @@ namespace {
 
 constexpr int kMaxWaves = 16;
 
-__device__ inline float wave_sum(float v) {
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-  return v;
-}
-
-// ------------------------------------------------------------------ c . K
-
-// cK[g, j] = c_b . K_j for the group's tokens and STOP, float32 accumulation.
-// One wave per column; lane l covers elements l, l+64, ...
-template <typename T>
-__global__ __launch_bounds__(256) void ck_kernel(const T* __restrict__ KQV, int64_t T_vis, int h,
-                                                 const float* __restrict__ ctx,
-                                                 const int32_t* __restrict__ grp_off,
-                                                 const int32_t* __restrict__ grp_img, int B,
-                                                 int max_group, float* __restrict__ cK, int ck_ld,
-                                                 int cols_per_block) {
-  const int g = blockIdx.y;
-  const int64_t g0 = grp_off[g], n = grp_off[g + 1] - g0;
-  const int b = grp_img[g];
-  if (g0 < 0 || n < 0 || n > max_group || g0 + n > T_vis || b < 0 || b >= B) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int per = h / 64;
-  float c[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i) c[i] = i < per ? ctx[(int64_t)b * h + lane + 64 * i] : 0.0f;
-  const int64_t ld = 3 * (int64_t)h;
-  const int j0 = blockIdx.x * cols_per_block;
-  for (int j = j0 + wave; j < j0 + cols_per_block && j <= n; j += 4) {
-    const T* krow = KQV + (j < n ? (g0 + j) : (T_vis + 1)) * ld;
-    float s = 0.0f;
-#pragma unroll
-    for (int i = 0; i < 16; ++i)
-      if (i < per) s = fmaf(c[i], (float)krow[lane + 64 * i], s);
-    s = wave_sum(s);
-    if (lane == 0) cK[(int64_t)g * ck_ld + j] = s;
-  }
-}
-
 // ------------------------------------------------------------------ the recurrence
 
-template <int CTRL, int ROW_MASK = 0xf>
-__device__ inline float dpp_mov(float old, float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(v), CTRL,
-                                                    ROW_MASK, 0xf, false));
-}
-
-// Wave-wide max / sum with DPP row shifts and row broadcasts (result in lane 63,
-// returned to every lane); a fixed combination order, so results are deterministic.
-__device__ inline float wave_max_dpp(float v) {
-  v = fmaxf(v, dpp_mov<0x111>(-INFINITY, v));        // row_shr:1
-  v = fmaxf(v, dpp_mov<0x112>(-INFINITY, v));        // row_shr:2
-  v = fmaxf(v, dpp_mov<0x114>(-INFINITY, v));        // row_shr:4
-  v = fmaxf(v, dpp_mov<0x118>(-INFINITY, v));        // row_shr:8
-  v = fmaxf(v, dpp_mov<0x142, 0xa>(-INFINITY, v));   // row_bcast:15
-  v = fmaxf(v, dpp_mov<0x143, 0xc>(-INFINITY, v));   // row_bcast:31
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
-}
-__device__ inline float wave_sum_dpp(float v) {
-  v += dpp_mov<0x111>(0.0f, v);
-  v += dpp_mov<0x112>(0.0f, v);
-  v += dpp_mov<0x114>(0.0f, v);
-  v += dpp_mov<0x118>(0.0f, v);
-  v += dpp_mov<0x142, 0xa>(0.0f, v);
-  v += dpp_mov<0x143, 0xc>(0.0f, v);
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
-}
-
 typedef float f32x32_t __attribute__((ext_vector_type(32)));
-
-__device__ inline int wave_min_dpp(int v) {
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x111, 0xf, 0xf, false));
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x112, 0xf, 0xf, false));
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x114, 0xf, 0xf, false));
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x118, 0xf, 0xf, false));
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x142, 0xa, 0xf, false));
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x143, 0xc, 0xf, false));
-  return __builtin_amdgcn_readlane(v, 63);
-}
 
 struct SelParams {
   const float* gram;
   int64_t gstride;
   int ld;
-  const float* cK;
-  int ck_ld;
   const int32_t* img_off;
   int B;
   const int32_t* grp_off;
@@ -194,7 +119,8 @@ __global__ __launch_bounds__(NT) void select_kernel(SelParams p) {
   const float* Bm = A + (int64_t)(n + 1) * p.ld;              // B row r at Bm + r * ld
   const int j = tid;
   const bool col = j <= n;
-  const float ck = col ? p.cK[(int64_t)g * p.ck_ld + j] : 0.0f;
+  const float* ckp = A + (int64_t)(2 * n + 2) * p.ld + j;   // the three parts of cK[j]
+  const float ck = col ? (ckp[0] + ckp[p.ld]) + ckp[2 * p.ld] : 0.0f;
   const float sigma = p.sigma;
   float* hist_j = hist + (col ? j : 0) * LT;
 
@@ -476,22 +402,25 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
     return hipGetLastError();
   }
   record_event(a.events, 0, stream);
-  hipError_t e = launch_gram_gemm(a.dtype, a.KQV, a.T_vis, a.h, a.grp_off, a.G, a.max_group,
-                                  a.gram, a.gram_group_stride, a.gram_ld, a.err, stream);
+  GramArgs ga;
+  ga.dtype = a.dtype;
+  ga.KQV = a.KQV;
+  ga.T_vis = a.T_vis;
+  ga.h = a.h;
+  ga.ctx = a.ctx;
+  ga.B = a.B;
+  ga.grp_off = a.grp_off;
+  ga.grp_img = a.grp_img;
+  ga.G = a.G;
+  ga.max_group = a.max_group;
+  ga.csplit = a.csplit;
+  ga.gram = a.gram;
+  ga.gram_group_stride = a.gram_group_stride;
+  ga.gram_ld = a.gram_ld;
+  ga.err = a.err;
+  hipError_t e = launch_gram_gemm(ga, stream);
   if (e != hipSuccess) return e;
   record_event(a.events, 1, stream);
-
-  const int cols_per_block = 32;
-  const dim3 ck_grid((a.max_group + 1 + cols_per_block - 1) / cols_per_block, a.G);
-  if (a.dtype == SP_BF16)
-    hipLaunchKernelGGL(ck_kernel<__bf16>, ck_grid, dim3(256), 0, stream, (const __bf16*)a.KQV,
-                       a.T_vis, a.h, a.ctx, a.grp_off, a.grp_img, a.B, a.max_group, a.cK, a.ck_ld,
-                       cols_per_block);
-  else
-    hipLaunchKernelGGL(ck_kernel<float>, ck_grid, dim3(256), 0, stream, (const float*)a.KQV,
-                       a.T_vis, a.h, a.ctx, a.grp_off, a.grp_img, a.B, a.max_group, a.cK, a.ck_ld,
-                       cols_per_block);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
 
   const bool trace = (a.flags & SP_TRACE) && a.trace && a.trace_steps > 0;
   if (trace) {
@@ -504,8 +433,6 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.gram = a.gram;
   p.gstride = a.gram_group_stride;
   p.ld = a.gram_ld;
-  p.cK = a.cK;
-  p.ck_ld = a.ck_ld;
   p.img_off = a.img_off;
   p.B = a.B;
   p.grp_off = a.grp_off;

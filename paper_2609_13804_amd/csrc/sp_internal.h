@@ -5,6 +5,8 @@
 #include <hip/hip_bf16.h>
 #include <stdint.h>
 #include <stddef.h>
+#include <limits.h>
+#include <math.h>
 
 #include "stepprune.h"
 
@@ -27,8 +29,49 @@ inline void record_event(const hipEvent_t* events, int i, hipStream_t stream) {
   if (events && events[i]) (void)hipEventRecord(events[i], stream);
 }
 
+// The first error wins and stays until stepprune_read_device_error clears it.
 __device__ inline void set_device_error(int32_t* err, int32_t code) {
   atomicCAS(err, 0, code);
+}
+
+// ---------------------------------------------------------------- wave reductions
+// DPP row shifts and row broadcasts combine a wave's 64 lanes in a fixed order
+// (deterministic results); the total is read from lane 63 and returned to every
+// lane.  Every lane of the wave must be active.
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ inline float dpp_mov(float old, float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(v), CTRL,
+                                                    ROW_MASK, 0xf, false));
+}
+
+__device__ inline float wave_max_dpp(float v) {
+  v = fmaxf(v, dpp_mov<0x111>(-INFINITY, v));        // row_shr:1
+  v = fmaxf(v, dpp_mov<0x112>(-INFINITY, v));        // row_shr:2
+  v = fmaxf(v, dpp_mov<0x114>(-INFINITY, v));        // row_shr:4
+  v = fmaxf(v, dpp_mov<0x118>(-INFINITY, v));        // row_shr:8
+  v = fmaxf(v, dpp_mov<0x142, 0xa>(-INFINITY, v));   // row_bcast:15
+  v = fmaxf(v, dpp_mov<0x143, 0xc>(-INFINITY, v));   // row_bcast:31
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+__device__ inline float wave_sum_dpp(float v) {
+  v += dpp_mov<0x111>(0.0f, v);
+  v += dpp_mov<0x112>(0.0f, v);
+  v += dpp_mov<0x114>(0.0f, v);
+  v += dpp_mov<0x118>(0.0f, v);
+  v += dpp_mov<0x142, 0xa>(0.0f, v);
+  v += dpp_mov<0x143, 0xc>(0.0f, v);
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+__device__ inline int wave_min_dpp(int v) {
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x111, 0xf, 0xf, false));
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x112, 0xf, 0xf, false));
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x114, 0xf, 0xf, false));
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x118, 0xf, 0xf, false));
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x142, 0xa, 0xf, false));
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x143, 0xc, 0xf, false));
+  return __builtin_amdgcn_readlane(v, 63);
 }
 
 // ---------------------------------------------------------------- GEMM launchers
@@ -38,19 +81,41 @@ __device__ inline void set_device_error(int32_t* err, int32_t code) {
 hipError_t launch_project_gemm(int dtype, const void* X, int64_t T_vis, const void* s_start,
                                const void* s_stop, const void* W, int d, int n_out, void* out,
                                hipStream_t stream);
-// Text projection: A = E_text [T_txt, d_text], B = W_text [h, d_text], fp32 output.
+// Text projection: A = E_text [T_txt, d_text], B = W_text [h, d_text], fp32
+// output split over K into text_split() partial products [split][T_txt][h],
+// which launch_text_pool adds in a fixed order.
+int text_split(int64_t T_txt, int h, int d_text);
 hipError_t launch_text_gemm(int dtype, const void* E, int64_t T_txt, const void* W, int d_text,
                             int h, float* out, hipStream_t stream);
-// Per-group Gram products of the projected rows (see select.hip for the layout).
-hipError_t launch_gram_gemm(int dtype, const void* KQV, int64_t T_vis, int h,
-                            const int32_t* grp_off, int G, int max_group, float* gram,
-                            int64_t gram_group_stride, int gram_ld, int32_t* err,
-                            hipStream_t stream);
+// Per-group Gram products of the projected rows (see select.hip for the
+// layout).  The text context of each image is first written as three rows of
+// the working dtype whose sum is exactly the float32 context (csplit,
+// [B][3][h]); they are the last three A-side rows of every group, so the
+// matrix cores also produce the three parts of cK = c [K; k_stop]^T.
+struct GramArgs {
+  int dtype;
+  const void* KQV;
+  int64_t T_vis;
+  int h;
+  const float* ctx;
+  int B;
+  const int32_t* grp_off;
+  const int32_t* grp_img;
+  int G;
+  int max_group;
+  void* csplit;
+  float* gram;
+  int64_t gram_group_stride;
+  int gram_ld;
+  int32_t* err;
+};
+constexpr int kGramExtraRows = 3;      // A-side rows of the context split
+hipError_t launch_gram_gemm(const GramArgs& a, hipStream_t stream);
 
 // ---------------------------------------------------------------- other launchers
-hipError_t launch_text_pool(const float* T, const int32_t* text_off, int B, int64_t T_txt, int h,
-                            float g_text, float ln_eps, float* ctx, int32_t* err,
-                            hipStream_t stream);
+hipError_t launch_text_pool(const float* T, int split, const int32_t* text_off, int B,
+                            int64_t T_txt, int h, float g_text, float ln_eps, float* ctx,
+                            int32_t* err, hipStream_t stream);
 
 struct SelectArgs {
   int dtype;
@@ -78,8 +143,7 @@ struct SelectArgs {
   float* gram;
   int64_t gram_group_stride;
   int gram_ld;
-  float* cK;             // [G, ck_ld]
-  int ck_ld;
+  void* csplit;          // [B][3][h] of the working dtype
   int32_t* grp_kept;     // [G, max_cap]
   int32_t* grp_count;    // [G]
   int32_t* err;
@@ -106,7 +170,5 @@ struct CompactArgs {
   int32_t* err;
 };
 hipError_t launch_compact(const CompactArgs& a, hipStream_t stream);
-
-hipError_t launch_clear_error(int32_t* err, hipStream_t stream);
 
 }  // namespace sp

@@ -2,9 +2,10 @@
 // Policy": text projection, LayerNorm, gain g_text), reduced to the pointer
 // query space:  c_b = g_text * mean_l LN(E_{b,l} W_text^T).
 //
-// The projection itself is a dense contraction (gemm.hip, float32 output);
-// this kernel normalises each projected row (no affine parameters, biased
-// variance, eps) and averages the rows of an image.  One workgroup per image;
+// The projection itself is a dense contraction (gemm.hip, float32 output,
+// split over K into `split` partial products that are added here in a fixed
+// order); this kernel normalises each projected row (no affine parameters,
+// biased variance, eps) and averages the rows of an image.  One workgroup per image;
 // each wave normalises whole rows with wave-level reductions and keeps a
 // private running sum, and the waves' sums are combined in a fixed order.
 #include "sp_internal.h"
@@ -19,6 +20,7 @@ __device__ inline float wsum(float v) {
   return v;
 }
 
+template <int SPLIT>
 __global__ __launch_bounds__(kPoolWaves * 64) void text_pool_kernel(
     const float* __restrict__ T, const int32_t* __restrict__ text_off, int64_t T_txt, int h,
     float g_text, float eps, float* __restrict__ ctx, int32_t* err) {
@@ -36,14 +38,25 @@ __global__ __launch_bounds__(kPoolWaves * 64) void text_pool_kernel(
 #pragma unroll
   for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
   for (int64_t r = r0 + wave; r < r1; r += kPoolWaves) {
+    // The K-split partial products of this row, all loads in flight at once,
+    // added in split order.
     const float* row = T + r * h;
+    float xp[SPLIT][16];
+#pragma unroll
+    for (int p = 0; p < SPLIT; ++p)
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        xp[p][i] = i < per ? row[(int64_t)p * T_txt * h + lane + 64 * i] : 0.0f;
     float x[16];
-    float s = 0.0f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      x[i] = i < per ? row[lane + 64 * i] : 0.0f;
-      s += x[i];
+      x[i] = xp[0][i];
+#pragma unroll
+      for (int p = 1; p < SPLIT; ++p) x[i] += xp[p][i];
     }
+    float s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s += x[i];
     const float mean = wsum(s) / (float)h;
     float q = 0.0f;
 #pragma unroll
@@ -71,12 +84,22 @@ __global__ __launch_bounds__(kPoolWaves * 64) void text_pool_kernel(
 
 }  // namespace
 
-hipError_t launch_text_pool(const float* T, const int32_t* text_off, int B, int64_t T_txt, int h,
-                            float g_text, float ln_eps, float* ctx, int32_t* err,
-                            hipStream_t stream) {
+hipError_t launch_text_pool(const float* T, int split, const int32_t* text_off, int B,
+                            int64_t T_txt, int h, float g_text, float ln_eps, float* ctx,
+                            int32_t* err, hipStream_t stream) {
   if (B == 0) return hipSuccess;
-  hipLaunchKernelGGL(text_pool_kernel, dim3(B), dim3(kPoolWaves * 64), 0, stream, T, text_off,
-                     T_txt, h, g_text, ln_eps, ctx, err);
+  const dim3 grid(B), block(kPoolWaves * 64);
+  switch (split) {
+    case 1: hipLaunchKernelGGL(text_pool_kernel<1>, grid, block, 0, stream, T, text_off, T_txt, h,
+                               g_text, ln_eps, ctx, err); break;
+    case 2: hipLaunchKernelGGL(text_pool_kernel<2>, grid, block, 0, stream, T, text_off, T_txt, h,
+                               g_text, ln_eps, ctx, err); break;
+    case 4: hipLaunchKernelGGL(text_pool_kernel<4>, grid, block, 0, stream, T, text_off, T_txt, h,
+                               g_text, ln_eps, ctx, err); break;
+    case 8: hipLaunchKernelGGL(text_pool_kernel<8>, grid, block, 0, stream, T, text_off, T_txt, h,
+                               g_text, ln_eps, ctx, err); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
