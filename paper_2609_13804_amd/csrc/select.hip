@@ -10,12 +10,10 @@
 //     cK = c [K; k_stop]^T,
 // and the history scores are sigma A[e, col(tau)].  A, B and cK are dense
 // contractions computed once per group on the matrix cores (gemm.hip), so a
-// step needs only the rows A[e, :] and B[e, :] of the newest history entry e:
-// one dependent load, then O(t * n) float32 FMAs.  One workgroup runs one
-// episode end to end, thread j owning candidate column j (j = n is STOP), so
-// no step ever leaves the compute unit: each thread keeps its column of the
-// history B rows in registers (LDS past RREG entries), every wave computes the
-// history softmax itself, reductions use DPP, and a step costs two barriers.
+// step needs only the row A[e, :] and the column values B[e, j] of the newest
+// history entry e: one dependent load, then O(t * n) float32 FMAs.  One
+// workgroup runs one episode end to end (select_kernel below), so no step
+// ever leaves the compute unit.
 //
 // Gram layout per group (float32, row stride ld): rows [0, n) A rows of the
 // tokens, row n the A row of START, rows [n+1, 2n+1) B rows of the tokens,
@@ -26,8 +24,6 @@
 
 namespace sp {
 namespace {
-
-constexpr int kMaxWaves = 16;
 
 // ------------------------------------------------------------------ the recurrence
 
@@ -45,9 +41,13 @@ struct SelParams {
   int64_t T_vis;
   int max_group;
   int max_cap;
-  int lds_tier;        // history entries per column held in LDS after the registers
+  int W;               // waves per workgroup; lane-owned columns [0, 64 W)
+  int lt;              // lane-owned history entries per thread in LDS after the registers
+  int ks;              // second-column history entries in LDS (multiple of 4)
   int alpha_ld;        // softmax weight array length (floats, multiple of 16)
+  int hcap;            // history capacity of the LDS index arrays (>= max_cap + 1)
   float sigma;
+  float c1;            // sigma * log2(e)
   float b_stop;
   uint32_t flags;
   int32_t* grp_kept;   // [G, max_cap] group-local kept indices, ascending
@@ -59,32 +59,135 @@ struct SelParams {
 };
 
 // Dynamic LDS of the recurrence (byte offsets), shared by host and device.
-// The LDS history tier is column-major, [column][lds_tier], so one 16-byte
-// read gives a thread four consecutive history entries of its column.
+//   hmain [64 W][lt]        lane-owned history past the registers (column-major)
+//   hsec  [ks / 4][64][4]   history of wave 0's second columns, four entries per lane
+//   alpha [alpha_ld]        softmax weights (unnormalised), written by wave 0
+//   sm    [4]               1 / softmax sum, STOP term of the older entries, newest weight
+//   hcol  [hcap]            history columns (START = n + 1)
+//   shist [hcap]            STOP column of the history B rows
+//   key   [2]               decision keys by step parity
+//   red   [16]              per-wave best and runner-up (tracing)
+//   cnt   [16]              end-of-episode counts
 struct SelLds {
-  int hist, arow, hcol, alpha, red, stop, total;
-  __host__ __device__ SelLds(int lds_tier, int max_group, int max_cap, int alpha_ld) {
-    hist = 0;
-    arow = hist + (max_group + 1) * lds_tier * 4;
-    hcol = arow + ((max_group + 2 + 3) & ~3) * 4;
-    alpha = (hcol + (max_cap + 2) * 4 + 15) & ~15;
-    red = alpha + alpha_ld * 4;
-    stop = red + kMaxWaves * 16;
-    total = stop + 16;
+  int hmain, hsec, alpha, sm, hcol, shist, key, red, cnt, total;
+  __host__ __device__ SelLds(int W, int lt, int ks, int alpha_ld, int hcap) {
+    hmain = 0;
+    hsec = hmain + 64 * W * lt * 4;
+    alpha = hsec + ks * 64 * 4;
+    sm = alpha + alpha_ld * 4;
+    hcol = sm + 16;
+    shist = (hcol + hcap * 4 + 15) & ~15;
+    key = (shist + hcap * 4 + 15) & ~15;
+    red = key + 16;
+    cnt = red + 16 * 16;
+    total = cnt + 16 * 4;
   }
 };
 
-// One workgroup runs one episode.  Thread j owns candidate column j (j = n is
-// STOP, j = n + 1 only loads the START column of A rows).  History B values of
-// its column: the first RREG in registers, the next lds_tier in LDS, any
-// further ones re-read from the Gram buffer in batches.
-template <int NT, int RREG, bool TRACE>
-__global__ __launch_bounds__(NT) void select_kernel(SelParams p) {
+// The value, recomputed where it is used: keeps rarely used addresses out of
+// the registers that hold the history across the step loop.
+__device__ __forceinline__ int opaque(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+// Workgroup barrier that orders LDS accesses only: outstanding global loads
+// stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Wave-wide max / sum, one fused DPP operation per stage: row shifts 1, 2, 4,
+// 8, then row broadcasts 15 and 31 (lanes without a source keep their value);
+// lane 63 ends with the result, returned to every lane.  A fixed combination
+// order, so results are deterministic.  The nops cover the VALU-write to DPP-
+// read hazard between stages.
+__device__ __forceinline__ float wave_max_fused(float v) {
+  asm volatile(
+      "s_nop 1\n\tv_max_f32_dpp %0, %0, %0 row_shr:1 row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\tv_max_f32_dpp %0, %0, %0 row_shr:2 row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\tv_max_f32_dpp %0, %0, %0 row_shr:4 row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\tv_max_f32_dpp %0, %0, %0 row_shr:8 row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\tv_max_f32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n\t"
+      "s_nop 1\n\tv_max_f32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf\n\t"
+      "s_nop 1"
+      : "+v"(v));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+__device__ __forceinline__ float wave_sum_fused(float v) {
+  asm volatile(
+      "s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_shr:1 row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_shr:2 row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_shr:4 row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_shr:8 row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n\t"
+      "s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf\n\t"
+      "s_nop 1"
+      : "+v"(v));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+// Two wave-wide sums in one DPP chain (independent stages interleaved).
+__device__ __forceinline__ void wave_sum2_fused(float& a, float& b) {
+  asm volatile(
+      "s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_shr:1 row_mask:0xf bank_mask:0xf\n\t"
+      "v_add_f32_dpp %1, %1, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_shr:2 row_mask:0xf bank_mask:0xf\n\t"
+      "v_add_f32_dpp %1, %1, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_shr:4 row_mask:0xf bank_mask:0xf\n\t"
+      "v_add_f32_dpp %1, %1, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_shr:8 row_mask:0xf bank_mask:0xf\n\t"
+      "v_add_f32_dpp %1, %1, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n\t"
+      "v_add_f32_dpp %1, %1, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n\t"
+      "s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf\n\t"
+      "v_add_f32_dpp %1, %1, %1 row_bcast:31 row_mask:0xc bank_mask:0xf\n\t"
+      "s_nop 1"
+      : "+v"(a), "+v"(b));
+  a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(a), 63));
+  b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(b), 63));
+}
+
+// Decision key: larger value first, then lower index (64-bit unsigned max).
+__device__ __forceinline__ uint64_t cand_key(float v, int idx) {
+  const uint32_t u = __float_as_uint(v);
+  const uint32_t ord = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((uint64_t)ord << 32) | (uint32_t)(0xffffffffu - (uint32_t)idx);
+}
+__device__ __forceinline__ float key_value(uint64_t k) {
+  const uint32_t ord = (uint32_t)(k >> 32);
+  return __uint_as_float((ord & 0x80000000u) ? (ord & 0x7fffffffu) : ~ord);
+}
+__device__ __forceinline__ int key_index(uint64_t k) {
+  return (int)(0xffffffffu - (uint32_t)k);
+}
+
+// One workgroup runs one episode with W waves.  Thread j < 64 W owns
+// candidate column j: its history B values are in registers (the first RREG
+// entries), then in LDS (lt entries), then re-read from the Gram buffer.
+// With SEC (W = 8, 513-576 tokens) lane c of wave 0 also owns column 512 + c,
+// with its history in LDS.  STOP is not a column: its history term is a dot
+// product of the weights with the STOP column of the history rows, reduced
+// inside the softmax.
+//
+// A step: every wave computes its columns' logits from the softmax weights in
+// LDS and folds its best candidate into the step's decision key (a 64-bit LDS
+// atomic max of value bits and inverted index, so ties go to the lower index
+// and STOP, index n, loses them); barrier; every wave reads the same decision;
+// each thread loads the chosen row's A and B values of its columns, and wave
+// 0 gathers the history scores from the chosen A row and writes the next
+// softmax into LDS; barrier.  The B values are first needed at the end of the
+// next step's logits, after the older history terms.
+template <int RREG, bool SEC, bool TRACE, int MAXT>
+__global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int g = blockIdx.x;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int nwaves = blockDim.x >> 6;
+  const int W = SEC ? 8 : p.W;
 
   const int64_t g0 = p.grp_off[g], g1 = p.grp_off[g + 1];
   const int n = (int)(g1 - g0);
@@ -106,36 +209,50 @@ __global__ __launch_bounds__(NT) void select_kernel(SelParams p) {
     }
   }
   const bool no_history = (p.flags & SP_NO_HISTORY) != 0;
-  const int LT = p.lds_tier;
-  const SelLds L(LT, p.max_group, p.max_cap, p.alpha_ld);
-  float* hist = reinterpret_cast<float*>(smem + L.hist);      // [max_group + 1][LT]
-  float* arow = reinterpret_cast<float*>(smem + L.arow);      // A row of the newest entry
-  int* hcol = reinterpret_cast<int*>(smem + L.hcol);          // A column of each history entry
-  float* alpha = reinterpret_cast<float*>(smem + L.alpha);    // softmax weights (zero padded)
-  float4* red = reinterpret_cast<float4*>(smem + L.red);      // per wave {v1, i1, v2, i2}
-  float* stop_sh = reinterpret_cast<float*>(smem + L.stop);
+  const int lt = p.lt, ks = p.ks;
+  const SelLds L(W, lt, ks, p.alpha_ld, p.hcap);
+  float* hmain = reinterpret_cast<float*>(smem + L.hmain);
+  float* hsec = reinterpret_cast<float*>(smem + L.hsec);
+  float* alpha = reinterpret_cast<float*>(smem + L.alpha);
+  float* sm = reinterpret_cast<float*>(smem + L.sm);
+  int* hcol = reinterpret_cast<int*>(smem + L.hcol);
+  float* shist = reinterpret_cast<float*>(smem + L.shist);
+  unsigned long long* key = reinterpret_cast<unsigned long long*>(smem + L.key);
+  float4* red = reinterpret_cast<float4*>(smem + L.red);
+  int* cnt = reinterpret_cast<int*>(smem + L.cnt);
 
-  const float* A = p.gram + (int64_t)g * p.gstride;           // A row r at A + r * ld
-  const float* Bm = A + (int64_t)(n + 1) * p.ld;              // B row r at Bm + r * ld
+  const int ld = p.ld;
+  const float* A = p.gram + (int64_t)g * p.gstride;          // A row r at A + r * ld
+  const float* Bm = A + (int64_t)(n + 1) * ld;               // B row r at Bm + r * ld
+  const float* CK = A + (int64_t)(2 * n + 2) * ld;           // the three parts of cK
   const int j = tid;
-  const bool col = j <= n;
-  const float* ckp = A + (int64_t)(2 * n + 2) * p.ld + j;   // the three parts of cK[j]
-  const float ck = col ? (ckp[0] + ckp[p.ld]) + ckp[2 * p.ld] : 0.0f;
-  const float sigma = p.sigma;
-  float* hist_j = hist + (col ? j : 0) * LT;
+  const bool mcol = j < n;
+  const int js = 512 + lane;                                 // second column (wave 0)
+  const bool scol = SEC && wave == 0 && js < n;
+  const float sigma = p.sigma, c1 = p.c1;
 
-  // Register-resident history of this column: up to 128 values in four
-  // separate 32-wide vector registers.  Reads use constant slots after
-  // unrolling; a write picks the vector with a uniform branch and the element
-  // with an indexed register move.  Separate variables rather than an array,
-  // and conditions the optimiser cannot prove exclusive, keep every access a
-  // register operation (an aggregate written at a dynamic index would be
-  // placed in scratch memory).
-  static_assert(RREG % 32 == 0 && RREG <= 128, "history registers come in 32-wide vectors");
+  auto ckv = [&](int c) { return (CK[c] + CK[ld + c]) + CK[2 * ld + c]; };
+  const float ck_main = mcol ? ckv(j) : 0.0f;
+  const float ck_sec = scol ? ckv(js) : 0.0f;
+  const float ck_stop = ckv(n);
+
+  for (int i = 0; i < lt; ++i) hmain[j * lt + i] = 0.0f;
+  if (SEC && wave == 0)
+    for (int i = 0; i < ks; i += 4)
+      *reinterpret_cast<float4*>(hsec + ((i >> 2) * 64 + lane) * 4) = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (tid < 2) key[tid] = 0ull;
+
+  // Lane-owned history values in 32-wide vector registers.  Reads use
+  // constant slots after unrolling; a write picks the vector with a uniform
+  // branch and the element with an indexed register move.  Separate variables
+  // and conditions the optimiser cannot prove exclusive keep every access a
+  // register operation.
+  static_assert(RREG % 32 == 0 && RREG <= 160, "history registers come in 32-wide vectors");
   constexpr int NV = RREG / 32;
-  f32x32_t h0{}, h1{}, h2{}, h3{};
+  f32x32_t h0{}, h1{}, h2{}, h3{}, h4{};
   auto hget = [&](int i) -> float {
-    return i < 32 ? h0[i & 31] : i < 64 ? h1[i & 31] : i < 96 ? h2[i & 31] : h3[i & 31];
+    return i < 32 ? h0[i & 31] : i < 64 ? h1[i & 31] : i < 96 ? h2[i & 31]
+         : i < 128 ? h3[i & 31] : h4[i & 31];
   };
   auto hput = [&](int pos, float x) {
     const int e = pos & 31;
@@ -144,198 +261,297 @@ __global__ __launch_bounds__(NT) void select_kernel(SelParams p) {
     if (NV > 1 && __builtin_amdgcn_readfirstlane(k == 1)) h1[e] = x;
     if (NV > 2 && __builtin_amdgcn_readfirstlane(k == 2)) h2[e] = x;
     if (NV > 3 && __builtin_amdgcn_readfirstlane(k == 3)) h3[e] = x;
+    if (NV > 4 && __builtin_amdgcn_readfirstlane(k == 4)) h4[e] = x;
   };
-  // A column of history entry lane + 64 k, for the first 256 entries.
-  int hc0 = lane == 0 ? n + 1 : 0, hc1 = 0, hc2 = 0, hc3 = 0;
+  // History column of entry lane + 64 k, for the first 256 entries.
+  int hc0 = 0, hc1 = 0, hc2 = 0, hc3 = 0;
 
-  // History entry 0 is START: row n of A and B, column n + 1 of A.
-  if (j <= n + 1) arow[j] = A[(int64_t)n * p.ld + j];
-  h0[0] = col ? Bm[(int64_t)n * p.ld + j] : 0.0f;
-  if (tid == 0) hcol[0] = n + 1;
-  bool selected = false;
-  int hl = 1;       // history length
+  // The newest history entry (position hl - 1): its column, its A values, and
+  // its B values, which are stored into the history one step later.
+  int ecol = n + 1;
+  float a_main = 0.0f, a_sec = 0.0f, a_stop = 0.0f;
+  float b_main = 0.0f, b_sec = 0.0f, b_stop = 0.0f;
+  int hl = 0;
+
+  // History softmax of the newest entry e (row r): unnormalised weights
+  // e_tau = exp(sigma (A[e, tau] - max)) into alpha, and into sm the reciprocal
+  // of their sum, the STOP term of the older entries (sum e_tau B[tau, STOP])
+  // and the newest entry's own weight.  Wave 0 only; the scores are gathered
+  // straight from the A row in the Gram buffer.
+  auto softmax_w0 = [&](const float* Ar) {
+    const int hpad = (hl + 15) & ~15;
+    float m, sum = 0.0f, s2 = 0.0f;
+    if (hl <= 256) {
+      const float x0 = lane < hl ? Ar[hc0] * c1 : -INFINITY;
+      const float x1 = 64 < hl && lane + 64 < hl ? Ar[hc1] * c1 : -INFINITY;
+      const float x2 = 128 < hl && lane + 128 < hl ? Ar[hc2] * c1 : -INFINITY;
+      const float x3 = 192 < hl && lane + 192 < hl ? Ar[hc3] * c1 : -INFINITY;
+      m = wave_max_fused(fmaxf(fmaxf(x0, x1), fmaxf(x2, x3)));
+      auto one = [&](int k, float x) {
+        const int tau = lane + 64 * k;
+        const float e = tau < hl ? __builtin_amdgcn_exp2f(x - m) : 0.0f;
+        sum += e;
+        s2 = fmaf(e, tau < hl - 1 ? shist[opaque(tau < hl - 1 ? tau : 0)] : 0.0f, s2);
+        if (tau < hpad) alpha[tau] = e;
+      };
+      one(0, x0);
+      if (64 < hpad) one(1, x1);
+      if (128 < hpad) one(2, x2);
+      if (192 < hpad) one(3, x3);
+    } else {
+      // longer histories: the scores are gathered again in each pass
+      m = -INFINITY;
+      for (int tau = lane; tau < hl; tau += 64) m = fmaxf(m, Ar[hcol[tau]] * c1);
+      m = wave_max_fused(m);
+      for (int tau = lane; tau < hpad; tau += 64) {
+        const float e = tau < hl ? __builtin_amdgcn_exp2f(Ar[hcol[tau]] * c1 - m) : 0.0f;
+        sum += e;
+        s2 = fmaf(e, tau < hl - 1 ? shist[tau < hl - 1 ? tau : 0] : 0.0f, s2);
+        alpha[tau] = e;
+      }
+    }
+    wave_sum2_fused(sum, s2);
+    if (lane == 0) {
+      sm[0] = __builtin_amdgcn_rcpf(sum);
+      sm[1] = s2;
+      sm[2] = __builtin_amdgcn_exp2f(Ar[ecol] * c1 - m);
+    }
+  };
+
+  // Load entry (row r, column c) as the newest: this thread's A value and the
+  // B values of its columns (left in flight); wave 0 also computes the next
+  // step's softmax.
+  auto load_entry = [&](int r, int c) {
+    const float* Ar = A + (int64_t)r * ld;
+    const float* Br = Bm + (int64_t)r * ld;
+    const int pos = hl;
+    a_main = mcol ? Ar[j] : 0.0f;
+    b_main = mcol ? Br[j] : 0.0f;
+    if (SEC) {
+      a_sec = scol ? Ar[js] : 0.0f;
+      b_sec = scol ? Br[js] : 0.0f;
+    }
+    a_stop = Ar[n];
+    b_stop = Br[n];
+    {
+      const int k = pos >> 6;
+      const bool mine = lane == (pos & 63);
+      if (__builtin_amdgcn_readfirstlane(k == 0) && mine) hc0 = c;
+      if (__builtin_amdgcn_readfirstlane(k == 1) && mine) hc1 = c;
+      if (__builtin_amdgcn_readfirstlane(k == 2) && mine) hc2 = c;
+      if (__builtin_amdgcn_readfirstlane(k == 3) && mine) hc3 = c;
+    }
+    if (tid == 0) hcol[pos] = c;
+    ecol = c;
+    hl = pos + 1;
+    if (wave == 0) softmax_w0(Ar);
+  };
+  // Store the newest entry's B values into the history (before the next one).
+  auto store_entry = [&]() {
+    const int pos = hl - 1;
+    if (pos < RREG) hput(pos, b_main);
+    else if (pos < RREG + lt) hmain[opaque(j) * lt + (pos - RREG)] = b_main;
+    if (SEC && wave == 0 && pos < ks) hsec[((pos >> 2) * 64 + opaque(lane)) * 4 + (pos & 3)] = b_sec;
+    if (tid == 0) shist[pos] = b_stop;
+  };
+
+  load_entry(n, n + 1);   // history entry 0 is START: row n of A and B, column n + 1
+  lds_barrier();
+  bool selected = false, sel_sec = false;
   int kept = 0;
-  __syncthreads();
 
   for (int t = 1; t <= cap; ++t) {
-    // ---- softmax of sigma * A[e, history]; every wave computes the same
-    // weights and writes the same values to the shared array, reading back only
-    // what it wrote itself.
-    const int hpad = (hl + 15) & ~15;
-    if (hl <= 256) {
-      float sv[4];
-      float m = -INFINITY;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        sv[k] = -INFINITY;
-        if (64 * k < hl) {
-          const int hc = k == 0 ? hc0 : k == 1 ? hc1 : k == 2 ? hc2 : hc3;
-          if (lane + 64 * k < hl) sv[k] = sigma * arow[hc];
-          m = fmaxf(m, sv[k]);
-        }
-      }
-      m = wave_max_dpp(m);
-      float sum = 0.0f;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        if (64 * k < hl) {
-          sv[k] = lane + 64 * k < hl ? expf(sv[k] - m) : 0.0f;
-          sum += sv[k];
-        }
-      }
-      sum = wave_sum_dpp(sum);
-#pragma unroll
-      for (int k = 0; k < 4; ++k)
-        if (lane + 64 * k < hpad) alpha[lane + 64 * k] = sv[k] / sum;
-    } else {
-      // Longer histories: scores are recomputed in each pass so that only
-      // final weights (identical in every wave) are ever written.
-      float m = -INFINITY;
-      for (int tau = lane; tau < hl; tau += 64) m = fmaxf(m, sigma * arow[hcol[tau]]);
-      m = wave_max_dpp(m);
-      float sum = 0.0f;
-      for (int tau = lane; tau < hl; tau += 64) sum += expf(sigma * arow[hcol[tau]] - m);
-      sum = wave_sum_dpp(sum);
-      for (int tau = lane; tau < hl; tau += 64) alpha[tau] = expf(sigma * arow[hcol[tau]] - m) / sum;
-      if (hl + lane < hpad) alpha[hl + lane] = 0.0f;
-    }
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
+    const int par = t & 1;
+    const float inv = sm[0], st = sm[1], e_new = sm[2];
 
-    // ---- pointer logit of this thread's candidate
-    float acc = col ? ck + arow[j] : 0.0f;
+    // ---- logits of the lane-owned columns: older entries from the history
+    // tiers (the newest entry's slots still hold zero), then the newest.
+    float acc = 0.0f, accb = 0.0f;   // two independent chains (even, odd entries)
+    {
+      // Weights come from LDS 16 at a time, the next 16 requested before the
+      // current 16 are used (alternating register sets, no copies).
+      const float4* a4 = reinterpret_cast<const float4*>(alpha);
+      float4 xa[2][4];
+      xa[0][0] = a4[0]; xa[0][1] = a4[1]; xa[0][2] = a4[2]; xa[0][3] = a4[3];
 #pragma unroll
-    for (int blk = 0; blk < RREG; blk += 16) {
-      if (blk < hl) {
-        const float4* a4 = reinterpret_cast<const float4*>(alpha + blk);
+      for (int bi = 0; bi < RREG / 16; ++bi) {
+        const int blk = bi * 16;
+        if (blk < hl) {
+          const int cur = bi & 1, nxt = cur ^ 1;
+          if (blk + 16 < RREG && blk + 16 < hl) {
+            xa[nxt][0] = a4[(blk + 16) / 4 + 0];
+            xa[nxt][1] = a4[(blk + 16) / 4 + 1];
+            xa[nxt][2] = a4[(blk + 16) / 4 + 2];
+            xa[nxt][3] = a4[(blk + 16) / 4 + 3];
+          }
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float4 x = a4[q];
-          acc = fmaf(x.x, hget(blk + 4 * q + 0), acc);
-          acc = fmaf(x.y, hget(blk + 4 * q + 1), acc);
-          acc = fmaf(x.z, hget(blk + 4 * q + 2), acc);
-          acc = fmaf(x.w, hget(blk + 4 * q + 3), acc);
+          for (int q = 0; q < 4; ++q) {
+            acc = fmaf(xa[cur][q].x, hget(blk + 4 * q + 0), acc);
+            accb = fmaf(xa[cur][q].y, hget(blk + 4 * q + 1), accb);
+            acc = fmaf(xa[cur][q].z, hget(blk + 4 * q + 2), acc);
+            accb = fmaf(xa[cur][q].w, hget(blk + 4 * q + 3), accb);
+          }
         }
       }
     }
     if (hl > RREG) {
-      const int lds_end = hl < RREG + LT ? hl : RREG + LT;
+      const int lend = hl < RREG + lt ? hl : RREG + lt;
+      const float* hj = hmain + opaque(j) * lt - RREG;
       int tau = RREG;
-      for (; tau + 4 <= lds_end; tau += 4) {
-        const float4 x = *reinterpret_cast<const float4*>(alpha + tau);
-        const float4 y = col ? *reinterpret_cast<const float4*>(hist_j + (tau - RREG))
-                             : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        acc = fmaf(x.x, y.x, acc);
-        acc = fmaf(x.y, y.y, acc);
-        acc = fmaf(x.z, y.z, acc);
-        acc = fmaf(x.w, y.w, acc);
+      for (; tau + 16 <= lend; tau += 16) {
+        float4 av[4], hv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          av[u] = *reinterpret_cast<const float4*>(alpha + tau + 4 * u);
+          hv[u] = *reinterpret_cast<const float4*>(hj + tau + 4 * u);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          acc = fmaf(av[u].x, hv[u].x, acc);
+          accb = fmaf(av[u].y, hv[u].y, accb);
+          acc = fmaf(av[u].z, hv[u].z, acc);
+          accb = fmaf(av[u].w, hv[u].w, accb);
+        }
       }
-      for (; tau < lds_end; ++tau) acc = fmaf(alpha[tau], col ? hist_j[tau - RREG] : 0.0f, acc);
-      for (; tau < hl; tau += 8) {
+      for (; tau < lend; tau += 4) {
+        const float4 av = *reinterpret_cast<const float4*>(alpha + tau);
+        const float4 hv = *reinterpret_cast<const float4*>(hj + tau);
+        acc = fmaf(av.x, hv.x, acc);
+        accb = fmaf(av.y, hv.y, accb);
+        acc = fmaf(av.z, hv.z, acc);
+        accb = fmaf(av.w, hv.w, accb);
+      }
+      for (tau = RREG + lt; tau < hl - 1; tau += 8) {
         float hv[8], av[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
           hv[u] = 0.0f;
           av[u] = 0.0f;
-          if (tau + u < hl) {
+          if (tau + u < hl - 1) {
             const int c = hcol[tau + u];
-            const int r = c == n + 1 ? n : c;
             av[u] = alpha[tau + u];
-            if (col) hv[u] = Bm[(int64_t)r * p.ld + j];
+            if (mcol) hv[u] = Bm[(int64_t)(c == n + 1 ? n : c) * ld + j];
           }
         }
 #pragma unroll
         for (int u = 0; u < 8; ++u) acc = fmaf(av[u], hv[u], acc);
       }
     }
-    float lj = sigma * acc;
-    if (j == n) {
-      lj += p.b_stop;
-      if (TRACE) *stop_sh = lj;
-    }
-    const bool valid = col && !selected;
+    acc = fmaf(e_new, b_main, acc + accb);
+    const float lj = sigma * (ck_main + a_main + acc * inv);
+    const float sp = fmaf(e_new, b_stop, st);
+    const float l_stop = sigma * (ck_stop + a_stop + sp * inv) + p.b_stop;
 
-    // ---- first maximal candidate of this wave (lowest index on ties)
+    // ---- wave 0's second columns: all their history in LDS (then global)
+    float ls = -INFINITY;
+    if (SEC && wave == 0) {
+      float acc2 = 0.0f, acc2b = 0.0f;
+      const int last = hl - 1;                 // the newest entry is added below
+      const int lend = last < ks ? last : ks;
+      int tau = 0;
+      for (; tau + 16 <= lend; tau += 16) {
+        float4 av[4], hv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          av[u] = *reinterpret_cast<const float4*>(alpha + tau + 4 * u);
+          hv[u] = *reinterpret_cast<const float4*>(hsec + (((tau >> 2) + u) * 64 + lane) * 4);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          acc2 = fmaf(av[u].x, hv[u].x, acc2);
+          acc2b = fmaf(av[u].y, hv[u].y, acc2b);
+          acc2 = fmaf(av[u].z, hv[u].z, acc2);
+          acc2b = fmaf(av[u].w, hv[u].w, acc2b);
+        }
+      }
+      for (; tau < lend; tau += 4) {
+        // entries past `last` in this block are zero in LDS and in alpha's padding
+        const float4 av = *reinterpret_cast<const float4*>(alpha + tau);
+        const float4 hv = *reinterpret_cast<const float4*>(hsec + ((tau >> 2) * 64 + lane) * 4);
+        acc2 = fmaf(av.x, hv.x, acc2);
+        acc2b = fmaf(av.y, hv.y, acc2b);
+        acc2 = fmaf(av.z, hv.z, acc2);
+        acc2b = fmaf(av.w, hv.w, acc2b);
+      }
+      for (tau = ks; tau < last; ++tau) {
+        const int c = hcol[tau];
+        const float hv = scol ? Bm[(int64_t)(c == n + 1 ? n : c) * ld + js] : 0.0f;
+        acc2 = fmaf(alpha[tau], hv, acc2);
+      }
+      acc2 = fmaf(e_new, b_sec, acc2 + acc2b);
+      ls = scol && !sel_sec ? sigma * (ck_sec + a_sec + acc2 * inv) : -INFINITY;
+    }
+
+    // ---- this wave's best candidate (lowest index on ties) into the key
+    const bool valid = mcol && !selected;
     const float v = valid ? lj : -INFINITY;
-    const float vmax = wave_max_dpp(v);
-    const uint64_t mask = __ballot(valid && v == vmax);
-    const int i1 = mask ? wave * 64 + __ffsll((unsigned long long)mask) - 1 : -1;
-    float v2 = -INFINITY;
-    int i2 = -1;
-    if (TRACE) {
-      const bool keep = valid && j != i1;
-      const float w2 = keep ? lj : -INFINITY;
-      v2 = wave_max_dpp(w2);
-      const uint64_t mask2 = __ballot(keep && w2 == v2);
-      i2 = mask2 ? wave * 64 + __ffsll((unsigned long long)mask2) - 1 : -1;
+    const float vmax = wave_max_fused(SEC ? fmaxf(v, ls) : v);
+    int i1 = -1;
+    if (vmax > -INFINITY) {
+      const uint64_t m1 = __ballot(valid && v == vmax);
+      if (m1) i1 = wave * 64 + __ffsll((unsigned long long)m1) - 1;
+      else if (SEC) i1 = 512 + __ffsll((unsigned long long)__ballot(ls == vmax)) - 1;
+      if (lane == 0) atomicMax(&key[par], (unsigned long long)cand_key(vmax, i1));
     }
-    if (lane == 0) red[wave] = make_float4(vmax, __int_as_float(i1), v2, __int_as_float(i2));
-    __syncthreads();
+    if (tid == 0 && l_stop > -INFINITY) atomicMax(&key[par], (unsigned long long)cand_key(l_stop, n));
+    if (TRACE) {
+      // runner-up of this wave: the best candidate other than i1
+      const float w1 = valid && j != i1 ? lj : -INFINITY;
+      const float w2 = SEC && js != i1 ? ls : -INFINITY;
+      const float v2 = wave_max_fused(fmaxf(w1, w2));
+      if (lane == 0) red[wave] = make_float4(vmax, __int_as_float(i1), v2, 0.0f);
+    }
+    lds_barrier();
 
-    // ---- merge the waves' candidates with one wave-wide reduction: lane w
-    // holds wave w's best (lanes 16 + w its runner-up); largest value, then
-    // lowest index.
-    float cv = -INFINITY;
-    int ci = -1;
-    if (lane < nwaves) {
-      const float4 r = red[lane];
-      cv = r.x;
-      ci = __float_as_int(r.y);
-    } else if (TRACE && lane >= 16 && lane < 16 + nwaves) {
-      const float4 r = red[lane - 16];
-      cv = r.z;
-      ci = __float_as_int(r.w);
-    }
-    const float bv = wave_max_dpp(ci >= 0 ? cv : -INFINITY);
-    const int a = wave_min_dpp(ci >= 0 && cv == bv ? ci : INT_MAX);   // STOP always competes
-    if (TRACE) {
-      // Runner-up over the same lanes (whole wave active for the reductions).
-      const bool rest = ci >= 0 && ci != a;
-      const float sv2 = wave_max_dpp(rest ? cv : -INFINITY);
-      const int si2 = wave_min_dpp(rest && cv == sv2 ? ci : INT_MAX);
-      if (tid == 0 && t <= p.trace_steps) {
+    // ---- the decision (every wave reads the same key)
+    const uint64_t kk = key[par];
+    const int a = kk ? key_index(kk) : n;       // no finite candidate: STOP
+    if (tid == 0) key[par ^ 1] = 0ull;          // next step's key (last read a step ago)
+    if (TRACE && tid == 0 && t <= p.trace_steps) {
+      // runner-up: the largest value among the candidates other than a
+      float r2 = a == n ? -INFINITY : l_stop;
+      for (int w = 0; w < W; ++w) {
+        const float4 r = red[w];
+        r2 = fmaxf(r2, __float_as_int(r.y) == a ? r.z : r.x);
+      }
       float* rec = p.trace + ((int64_t)g * p.trace_steps + (t - 1)) * 4;
       rec[0] = __int_as_float(a == n ? -1 : a);
-      rec[1] = bv;
-      rec[2] = si2 != INT_MAX ? sv2 : -INFINITY;
-      rec[3] = *stop_sh;
-      }
+      rec[1] = kk ? key_value(kk) : l_stop;
+      rec[2] = r2;
+      rec[3] = l_stop;
     }
     if (a == n) break;
     ++kept;
     if (j == a) selected = true;
+    if (SEC && js == a) sel_sec = true;
     if (!no_history) {
-      // Append a: its A row becomes the current row, its B row the newest
-      // history entry of every column.
-      if (tid == 0) hcol[hl] = a;
-      {
-        const int k = hl >> 6;
-        const bool mine = lane == (hl & 63);
-        if (__builtin_amdgcn_readfirstlane(k == 0) && mine) hc0 = a;
-        if (__builtin_amdgcn_readfirstlane(k == 1) && mine) hc1 = a;
-        if (__builtin_amdgcn_readfirstlane(k == 2) && mine) hc2 = a;
-        if (__builtin_amdgcn_readfirstlane(k == 3) && mine) hc3 = a;
-      }
-      if (j <= n + 1) arow[j] = A[(int64_t)a * p.ld + j];
-      const float bv_new = col ? Bm[(int64_t)a * p.ld + j] : 0.0f;
-      if (hl < RREG) hput(hl, bv_new);
-      else if (hl < RREG + LT && col) hist_j[hl - RREG] = bv_new;
-      ++hl;
+      store_entry();
+      load_entry(a, a);
     }
-    __syncthreads();
+    lds_barrier();     // the next softmax is in LDS
   }
 
-  // ---- native order (Algorithm 1 step 4): ascending positions of the set bits
+  // ---- native order (Algorithm 1 step 4): ascending positions of the set
+  // bits, lane-owned columns first, then wave 0's second columns.
   __syncthreads();
-  int32_t* red32 = reinterpret_cast<int32_t*>(red);
-  const uint64_t ballot = __ballot(j < n && selected);
-  if (lane == 0) red32[wave] = __popcll(ballot);
+  const uint64_t ballot = __ballot(mcol && selected);
+  if (lane == 0) cnt[wave] = __popcll(ballot);
   __syncthreads();
-  int before = 0;
-  for (int w = 0; w < wave; ++w) before += red32[w];
-  if (j < n && selected) {
+  int before = 0, total = 0;
+  for (int w = 0; w < W; ++w) {
+    if (w < wave) before += cnt[w];
+    total += cnt[w];
+  }
+  if (mcol && selected) {
     const int pos = before + __popcll(ballot & ((1ull << lane) - 1ull));
     p.grp_kept[(int64_t)g * p.max_cap + pos] = j;
+  }
+  if (SEC && wave == 0) {
+    const uint64_t sb = __ballot(scol && sel_sec);
+    if (scol && sel_sec) {
+      const int pos = total + __popcll(sb & ((1ull << lane) - 1ull));
+      p.grp_kept[(int64_t)g * p.max_cap + pos] = js;
+    }
   }
   if (tid == 0) {
     p.grp_count[g] = kept;
@@ -441,7 +657,6 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.T_vis = a.T_vis;
   p.max_group = a.max_group;
   p.max_cap = a.max_cap;
-  p.sigma = 1.0f / sqrtf((float)a.h);
   p.b_stop = a.b_stop;
   p.flags = a.flags;
   p.grp_kept = a.grp_kept;
@@ -451,43 +666,70 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.trace_steps = trace ? a.trace_steps : 0;
   p.err = a.err;
 
-  const int threads = (a.max_group + 2 + 63) / 64 * 64;
-  const int nt_class = threads <= 320 ? 320 : threads <= 640 ? 640 : 1024;
-  const int need = a.max_cap + 1;                       // longest possible history
-  // History registers per thread: the VGPR budget is 512 / (waves per SIMD),
-  // so 16 waves allow 64 values, 10 waves 96 and 5 waves 128.
-  const int rmax = nt_class == 1024 ? 64 : nt_class == 640 ? 96 : 128;
-  int rreg = (need + 31) / 32 * 32;
-  if (rreg > rmax) rreg = rmax;
-  p.alpha_ld = (int)align_up((size_t)a.max_cap + 2, 16);
-  const size_t fixed = (size_t)SelLds(0, a.max_group, a.max_cap, p.alpha_ld).total;
-  const size_t per_entry = (size_t)(a.max_group + 1) * 4;   // one LDS history entry, all columns
-  size_t lt_max = fixed < (size_t)kLdsBytes ? ((size_t)kLdsBytes - fixed) / per_entry : 0;
-  // Column stride of 8k + 4 floats keeps the 16-byte reads of eight
-  // consecutive columns on distinct banks.
-  lt_max = lt_max >= 4 ? (lt_max - 4) / 8 * 8 + 4 : 0;
-  size_t lt = 0;
-  if (need > rreg) {
-    lt = (size_t)(need - rreg + 3) / 8 * 8 + 4;   // smallest 8k + 4 >= the entries needed
-    if (lt > lt_max) lt = lt_max;
+  // Waves: one lane per token column up to 512 columns (2 waves per SIMD, 256
+  // registers each); 513-576 columns keep 8 waves and give wave 0 a second
+  // column per lane; larger groups take 16 waves (128 registers each).
+  const int mg = a.max_group > 0 ? a.max_group : 1;
+  int W;
+  bool sec = false;
+  if (mg <= 512) {
+    W = (mg + 63) / 64;
+  } else if (mg <= 576) {
+    W = 8;
+    sec = true;
+  } else {
+    W = (mg + 63) / 64;
   }
-  p.lds_tier = (int)lt;
-  const size_t lds = (size_t)SelLds((int)lt, a.max_group, a.max_cap, p.alpha_ld).total;
+  const bool wide = W > 8;
+  const int need = a.max_cap + 1;                       // longest possible history
+  int rreg = wide ? 32 : need <= 64 ? 64 : need <= 128 ? 128 : 160;
+  p.W = W;
+  p.hcap = (int)align_up((size_t)need + 1, 4);
+  p.alpha_ld = (int)align_up((size_t)need, 16);
+  p.sigma = 1.0f / sqrtf((float)a.h);
+  p.c1 = p.sigma * 1.4426950408889634f;
+  // LDS: fixed arrays, then wave 0's second-column history (all of it if it
+  // fits), then the lane-owned tier past the registers; entries beyond either
+  // are read again from the Gram buffer.
+  const size_t fixed = (size_t)SelLds(W, 0, 0, p.alpha_ld, p.hcap).total;
+  size_t room = fixed < (size_t)kLdsBytes ? (size_t)kLdsBytes - fixed : 0;
+  int ks = 0;
+  if (sec) {
+    ks = (need + 3) / 4 * 4;
+    const size_t per = 64 * 4;
+    if ((size_t)ks * per > room) ks = (int)(room / per) / 4 * 4;
+    room -= (size_t)ks * per;
+  }
+  int lt = 0;
+  if (need > rreg) {
+    lt = (need - rreg + 3) / 8 * 8 + 4;                 // smallest 8k + 4 >= the entries needed
+    const size_t per = (size_t)64 * W * 4;
+    size_t lt_max = room / per;
+    // Column stride of 8k + 4 floats keeps the 16-byte reads of eight
+    // consecutive columns on distinct banks.
+    lt_max = lt_max >= 4 ? (lt_max - 4) / 8 * 8 + 4 : 0;
+    if ((size_t)lt > lt_max) lt = (int)lt_max;
+  }
+  p.lt = lt;
+  p.ks = ks;
+  const size_t lds = (size_t)SelLds(W, lt, ks, p.alpha_ld, p.hcap).total;
+  if (lds > (size_t)kLdsBytes) return hipErrorInvalidValue;
 
   const void* fn = nullptr;
-#define SP_PICK(NT, RR)                                                             \
-  if (nt_class == NT && rreg == RR)                                                 \
-    fn = trace ? (const void*)select_kernel<NT, RR, true> : (const void*)select_kernel<NT, RR, false>;
-  SP_PICK(320, 32) SP_PICK(320, 64) SP_PICK(320, 96) SP_PICK(320, 128)
-  SP_PICK(640, 32) SP_PICK(640, 64) SP_PICK(640, 96)
-  SP_PICK(1024, 32) SP_PICK(1024, 64)
+#define SP_PICK(RR, SEC, MAXT)                                                           \
+  if (rreg == RR && sec == SEC && (MAXT == 1024) == wide)                                \
+    fn = trace ? (const void*)select_kernel<RR, SEC, true, MAXT>                         \
+               : (const void*)select_kernel<RR, SEC, false, MAXT>;
+  SP_PICK(64, false, 512) SP_PICK(128, false, 512) SP_PICK(160, false, 512)
+  SP_PICK(64, true, 512) SP_PICK(128, true, 512) SP_PICK(160, true, 512)
+  SP_PICK(32, false, 1024)
 #undef SP_PICK
   if (!fn) return hipErrorInvalidValue;
   record_event(a.events, 2, stream);
   if ((e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) != hipSuccess)
     return e;
   void* kargs[] = {&p};
-  if ((e = hipLaunchKernel(fn, dim3(a.G), dim3(threads), kargs, lds, stream)) != hipSuccess) return e;
+  if ((e = hipLaunchKernel(fn, dim3(a.G), dim3(64 * W), kargs, lds, stream)) != hipSuccess) return e;
   record_event(a.events, 3, stream);
 
   hipLaunchKernelGGL(finalize_kernel, dim3(a.B), dim3(256), 0, stream, a.img_off, a.B, a.grp_off,

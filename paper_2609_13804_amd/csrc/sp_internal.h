@@ -34,46 +34,6 @@ __device__ inline void set_device_error(int32_t* err, int32_t code) {
   atomicCAS(err, 0, code);
 }
 
-// ---------------------------------------------------------------- wave reductions
-// DPP row shifts and row broadcasts combine a wave's 64 lanes in a fixed order
-// (deterministic results); the total is read from lane 63 and returned to every
-// lane.  Every lane of the wave must be active.
-template <int CTRL, int ROW_MASK = 0xf>
-__device__ inline float dpp_mov(float old, float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(v), CTRL,
-                                                    ROW_MASK, 0xf, false));
-}
-
-__device__ inline float wave_max_dpp(float v) {
-  v = fmaxf(v, dpp_mov<0x111>(-INFINITY, v));        // row_shr:1
-  v = fmaxf(v, dpp_mov<0x112>(-INFINITY, v));        // row_shr:2
-  v = fmaxf(v, dpp_mov<0x114>(-INFINITY, v));        // row_shr:4
-  v = fmaxf(v, dpp_mov<0x118>(-INFINITY, v));        // row_shr:8
-  v = fmaxf(v, dpp_mov<0x142, 0xa>(-INFINITY, v));   // row_bcast:15
-  v = fmaxf(v, dpp_mov<0x143, 0xc>(-INFINITY, v));   // row_bcast:31
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
-}
-
-__device__ inline float wave_sum_dpp(float v) {
-  v += dpp_mov<0x111>(0.0f, v);
-  v += dpp_mov<0x112>(0.0f, v);
-  v += dpp_mov<0x114>(0.0f, v);
-  v += dpp_mov<0x118>(0.0f, v);
-  v += dpp_mov<0x142, 0xa>(0.0f, v);
-  v += dpp_mov<0x143, 0xc>(0.0f, v);
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
-}
-
-__device__ inline int wave_min_dpp(int v) {
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x111, 0xf, 0xf, false));
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x112, 0xf, 0xf, false));
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x114, 0xf, 0xf, false));
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x118, 0xf, 0xf, false));
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x142, 0xa, 0xf, false));
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x143, 0xc, 0xf, false));
-  return __builtin_amdgcn_readlane(v, 63);
-}
-
 // ---------------------------------------------------------------- GEMM launchers
 // C[m, n] = sum_k A[m, k] * B[n, k]  (both operands K-contiguous), fp32 accumulate.
 
