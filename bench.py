@@ -9,12 +9,17 @@ the LLaVA-1.5-shaped one: 16 images x 576 tokens x 4096, bf16, selector
 hidden width 1024, cap 192, STOP bias set so that the mean retained count is
 about 64, compaction into 576 + 64 prefill rows.
 
-Prints one JSON line.  The roofline object covers the kernel with the largest
-average duration, timed with HIP events that the library records around it
-on the launch stream; the CPU baseline is the float64 oracle timed on this
-host's cores over a bounded sample of the same batch.
+Two timed passes over K steps each: one stream running the batches one after
+another (per-stage and per-kernel times from HIP events the library records on
+that stream; reported as "single_stream"), then S streams taking consecutive
+batches in turn, each with its own outputs and workspaces, so that one batch's
+projection runs beside another batch's recurrence ("value", the whole job's
+throughput).  Prints one JSON line.  The roofline object covers the kernel with
+the largest average duration in the single-stream pass; the CPU baseline is
+the float64 oracle timed on this host's cores over a bounded sample of the
+same batch.
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload llava15_bf16]
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--streams 3] [--workload llava15_bf16]
 """
 import argparse
 import ctypes
@@ -165,6 +170,9 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llava15_bf16")
+    ap.add_argument("--streams", type=int, default=3,
+                    help="consecutive batches go round-robin to this many streams, each with its "
+                         "own outputs and workspaces (1: one stream, one batch after another)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle work for the CPU baseline sample")
@@ -265,6 +273,38 @@ def main(argv=None):
                 "algorithmic": f"{amount:.6g} {'TFLOP' if unit == 'TFLOP/s' else 'GB'} per launch"}
 
     elapsed = t1 - t0
+    single = {"images_per_s": round(K * s.B / elapsed, 2), "ms_per_step": round(1e3 * elapsed / K, 4)}
+
+    # Pipelined pass: batch k on stream k mod S, so one batch's projection and
+    # Gram products run on the compute units that another batch's recurrence
+    # (one workgroup per episode) leaves free.  Each stream owns its outputs
+    # and workspaces; the inputs are shared read-only.
+    S = max(1, args.streams)
+    if S > 1:
+        runs = [run] + [run.sibling() for _ in range(S - 1)]
+        streams = [torch.cuda.Stream() for _ in range(S)]     # default priority
+        def issue(k):
+            r, st = runs[k % S], streams[k % S].cuda_stream
+            r.project(st)
+            r.select(st)
+            if r.out is not None:
+                r.compact(st)
+        for k in range(max(args.warmup, S)):
+            issue(k)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(K):
+            issue(k)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        errs = [e for r in runs for e in r.device_errors()]
+        if any(errs):
+            raise RuntimeError(f"device error words {errs}")
+        for r in runs[1:]:
+            if not (torch.equal(r.kept_idx, run.kept_idx) and
+                    (r.out is None or torch.equal(r.out, run.out))):
+                raise RuntimeError("streams disagree on the same batch")
+        elapsed = t1 - t0
     value = K * s.B / elapsed
     out = {
         "metric": METRIC,
@@ -280,12 +320,13 @@ def main(argv=None):
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic",
-        "config": {"workload": w.name, "images": s.B, "groups": s.G,
+        "config": {"workload": w.name, "images": s.B, "groups": s.G, "streams": S,
                    "tokens": int(s.T_vis), "d": w.d, "h": w.h, "text_tokens": int(s.T_txt),
                    "layout": w.layout, "b_stop": b_stop,
                    "kept_mean_per_image": round(float(kept_b.mean()), 3),
                    "selection_steps": int(sum(steps_g)),
                    "longest_episode_steps": int(max(steps_g))},
+        "single_stream": single,
         "stages_us": {k: round(v, 2) for k, v in stages.items()},
         "kernels_us": {k: round(v, 2) for k, v in kernels.items()},
         "selection_steps_per_s": round(sum(steps_g) / (stages["select"] * 1e-6), 1),

@@ -3,6 +3,7 @@
 Plumbing only: torch allocates HBM and provides the stream; every stage runs
 in libstepprune's kernels through the binding.
 """
+import copy
 from dataclasses import dataclass
 from typing import Dict, Optional
 
@@ -72,31 +73,43 @@ class DeviceRun:
                            kept_total=int(kept_off[-1]))
         s = self.sizes
         self.dims = sp.dims(w.d, w.d_text, w.h, sp.SP_F32 if w.dtype == "f32" else sp.SP_BF16)
-        self.KQV = torch.empty((s.T_vis + 2, 3 * w.h), dtype=tdt, device=dev)
-        self.ctx = torch.empty((s.B, w.h), dtype=torch.float32, device=dev)
-        self.kept_idx = torch.full((max(1, s.kept_total),), -1, dtype=torch.int32, device=dev)
-        self.kept_cnt = torch.zeros(s.B, dtype=torch.int32, device=dev)
-        self.grp_cnt = torch.zeros(max(1, s.G), dtype=torch.int32, device=dev)
-        self.trace = (torch.empty((s.G, trace_steps, 4), dtype=torch.float32, device=dev)
-                      if trace_steps > 0 else None)
         if w.layout == "padded":
             self.layout_code = sp.SP_LAYOUT_PADDED
             self.rows_per_image = layout.rows_per_image
             self.out_rows = s.B * layout.rows_per_image
-            self.seq_info = torch.zeros(s.B, dtype=torch.int32, device=dev)
         else:
             self.layout_code = sp.SP_LAYOUT_PACKED
             self.rows_per_image = 0
             self.out_rows = s.kept_total + s.T_txt
-            self.seq_info = torch.zeros(s.B + 1, dtype=torch.int32, device=dev)
-        self.out = (torch.zeros((self.out_rows, w.d), dtype=tdt, device=dev)
-                    if w.d_text == w.d else None)
         nb = lambda which: sp.stepprune_workspace_bytes(which, self.dims, s.T_vis, s.T_txt, s.B,
                                                         s.G, s.max_group, s.max_cap)
         self.ws_bytes = [nb(sp.STAGE_PROJECT), nb(sp.STAGE_SELECT), nb(sp.STAGE_COMPACT)]
         if min(self.ws_bytes) == 0:
             raise ValueError("workspace size query rejected the sizes")
+        self._alloc_outputs()
+
+    def _alloc_outputs(self):
+        """Outputs and workspaces (zero-filled workspaces: their error words start clear)."""
+        s, w, dev, tdt = self.sizes, self.w, self.X.device, self.X.dtype
+        self.KQV = torch.empty((s.T_vis + 2, 3 * w.h), dtype=tdt, device=dev)
+        self.ctx = torch.empty((s.B, w.h), dtype=torch.float32, device=dev)
+        self.kept_idx = torch.full((max(1, s.kept_total),), -1, dtype=torch.int32, device=dev)
+        self.kept_cnt = torch.zeros(s.B, dtype=torch.int32, device=dev)
+        self.grp_cnt = torch.zeros(max(1, s.G), dtype=torch.int32, device=dev)
+        self.trace = (torch.empty((s.G, self.trace_steps, 4), dtype=torch.float32, device=dev)
+                      if self.trace_steps > 0 else None)
+        self.seq_info = torch.zeros(s.B + (self.layout_code == sp.SP_LAYOUT_PACKED), dtype=torch.int32,
+                                    device=dev)
+        self.out = (torch.zeros((self.out_rows, w.d), dtype=tdt, device=dev)
+                    if w.d_text == w.d else None)
         self.ws = [torch.zeros(n, dtype=torch.uint8, device=dev) for n in self.ws_bytes]
+
+    def sibling(self):
+        """Another run of the same batch that shares the inputs (read only) and has
+        outputs and workspaces of its own, for work on a second stream."""
+        other = copy.copy(self)
+        other._alloc_outputs()
+        return other
 
     # ---------------------------------------------------------------- stages
     def project(self, stream=None, g_text: float = 1.0, ln_eps: float = 1e-5, events=None):
