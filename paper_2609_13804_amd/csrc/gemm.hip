@@ -186,9 +186,11 @@ __device__ __forceinline__ void gemm_block(const ARows& ar, const BRows& br, int
 // (global_load_lds_dwordx4: one wave instruction fills 1 KiB = 16 rows x 64
 // bytes) through a ring of S stage buffers, loads running S - 1 stages ahead
 // of the matrix cores.  Within a 64-byte row the four 16-byte chunks are
-// stored XOR-swizzled (chunk c of row r at slot c ^ ((r >> 1) & 3)), which the
-// load realises by choosing each lane's source address, so that the 16-byte
-// fragment reads of consecutive rows hit distinct banks.  Rows past M (N) are
+// stored XOR-swizzled (chunk c of row r at slot c ^ ((r >> 2) & 3)), which the
+// load realises by choosing each lane's source address: a 16-byte fragment
+// read serves 16 lanes (16 consecutive rows, 4 rows per 256-byte pass over the
+// 64 banks) at a time, and rows 4 apart take different slots, so no two lanes
+// of a pass share a bank.  Rows past M (N) are
 // clamped to the last valid row and their results are not stored.
 constexpr int kBM = 256, kBN = 256, kBK = 32, kStages = 4;
 constexpr int kOpBytes = kBM * kBK * 2;                // one operand tile, 16 KiB
@@ -211,7 +213,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 // Byte offset of (row, 16-byte chunk) in a swizzled operand tile (64-byte rows).
 __device__ __forceinline__ int swz(int row, int chunk) {
-  return row * 64 + ((chunk ^ ((row >> 1) & 3)) << 4);
+  return row * 64 + ((chunk ^ ((row >> 2) & 3)) << 4);
 }
 
 template <typename OutT, class ARows, class BRows>
@@ -224,10 +226,10 @@ __device__ __forceinline__ void gemm_bf16_256(const ARows& ar, const BRows& br, 
   const int wm = wave >> 1, wn = wave & 1;
 
   // This wave loads 16-row groups wave + 4 i (i < 4) of both operand tiles;
-  // lane (rl = lane / 4, slot = lane % 4) fetches chunk slot ^ ((rl >> 1) & 3)
+  // lane (rl = lane / 4, slot = lane % 4) fetches chunk slot ^ ((rl >> 2) & 3)
   // of row rl.
   const int rl = lane >> 2;
-  const int chunk = (lane & 3) ^ ((rl >> 1) & 3);
+  const int chunk = (lane & 3) ^ ((rl >> 2) & 3);
   const __bf16* pa[4];
   const __bf16* pb[4];
 #pragma unroll

@@ -1,0 +1,67 @@
+"""Group sizes at the edges of the selection kernel's launch shapes, checked
+element by element against the oracle (tests/parity.py protocol):
+
+  * up to 512 tokens: one lane per token column;
+  * 513-576 tokens: wave 0's lanes also own the columns past 512;
+  * more than 576 tokens: 16 waves with fewer history registers per lane;
+
+with caps that keep the history in registers, and caps that push it through
+the LDS rows and the re-read tier.  Each case runs the untraced kernel (the
+benchmark's) and the traced one, which must take the same decisions.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_13804_amd import workloads as W
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+
+CASES = [
+    # (name, cfg id, tokens per image, cap, STOP bias)
+    ("wide_1000", 105, (1000, 700, 33), 48, -math.inf),
+    ("wide_1000_stop", 105, (1000, 700, 33), 48, 0.25),
+    ("second_cols_576", 106, (576, 513, 512, 65), 64, 0.25),
+    ("second_cols_deep", 107, (513, 520), 300, -math.inf),
+    ("lanes_512", 108, (512, 448, 64, 1), 40, 0.1),
+]
+
+
+def _workload(name, cfg, tokens, cap):
+    return W.Workload(name, cfg, batch=len(tokens), d=256, d_text=256, h=128, dtype="bf16",
+                      text_len=5, tokens=tokens, cap=cap, layout="padded",
+                      description="group-shape edge case")
+
+
+@pytest.mark.parametrize("name,cfg,tokens,cap,b_stop", CASES, ids=[c[0] for c in CASES])
+def test_group_shape(gpu_lib, name, cfg, tokens, cap, b_stop):
+    from paper_2609_13804_amd.runner import DeviceRun
+    from paper_2609_13804_amd import binding as sp
+    w = _workload(name, cfg, tokens, cap)
+    lay = W.make_layout(w)
+    inp = W.make_inputs(w)
+    sizes = np.diff(lay.grp_off)
+    steps = int(max(min(int(c), int(n)) for c, n in zip(lay.grp_cap, sizes))) + 1
+    run = DeviceRun(w, inp, lay, b_stop, trace_steps=steps)
+    run.project()
+    run.select(flags=0)
+    run.compact()
+    torch.cuda.synchronize()
+    assert run.device_errors() == [0, 0, 0]
+    plain = run.kept_lists()
+    run.select(flags=sp.SP_TRACE)
+    torch.cuda.synchronize()
+    assert run.device_errors() == [0, 0, 0]
+    assert run.kept_lists() == plain
+    actions = run.trace_actions()
+    KQV = run.KQV.double().cpu().numpy()
+    ctx = run.ctx.double().cpu().numpy()
+    rep = parity.check_selection(KQV, ctx, lay.grp_off, lay.grp_img, lay.grp_cap, b_stop, w.h,
+                                 actions, run.trace.cpu().numpy(), w.dtype)
+    assert plain == parity.kept_from_actions(actions, lay.grp_off, lay.grp_img, lay.img_off,
+                                             lay.batch)
+    print(f"{name}: {rep.episodes} episodes, {rep.steps} steps, {rep.exempt_steps} exempt, "
+          f"max logit err {rep.max_logit_err:.2e}, kept {[len(k) for k in plain]}")
