@@ -73,9 +73,11 @@ constexpr int kGramExtraRows = 3;      // A-side rows of the context split
 hipError_t launch_gram_gemm(const GramArgs& a, hipStream_t stream);
 
 // ---------------------------------------------------------------- other launchers
-hipError_t launch_text_pool(const float* T, int split, const int32_t* text_off, int B,
-                            int64_t T_txt, int h, float g_text, float ln_eps, float* ctx,
-                            int32_t* err, hipStream_t stream);
+// LayerNorm of every projected text row (in place over partial product 0)
+// and the per-image mean with gain: ctx[b] = g_text * mean_l LN(T_l).
+hipError_t launch_text_pool(float* T, int split, const int32_t* text_off, int B, int64_t T_txt,
+                            int h, float g_text, float ln_eps, float* ctx, int32_t* err,
+                            hipStream_t stream);
 
 struct SelectArgs {
   int dtype;
