@@ -43,7 +43,7 @@ struct SelParams {
   int max_cap;
   int W;               // waves per workgroup; lane-owned columns [0, 64 W)
   int lt;              // lane-owned history entries per thread in LDS after the registers
-  int ks;              // second-column history entries in LDS (multiple of 4)
+  int ks;              // second-column history entries in LDS (multiple of 64)
   int alpha_ld;        // softmax weight array length (floats, multiple of 16)
   int hcap;            // history capacity of the LDS index arrays (>= max_cap + 1)
   float sigma;
@@ -60,8 +60,10 @@ struct SelParams {
 
 // Dynamic LDS of the recurrence (byte offsets), shared by host and device.
 //   hmain [64 W][lt]        lane-owned history past the registers (column-major)
-//   hsec  [ks / 4][64][4]   history of wave 0's second columns, four entries per lane
-//   alpha [alpha_ld]        softmax weights (unnormalised), written by wave 0
+//   hsec  [ks / 16][64][4][4]  history of the second columns: entry 16 k + 4 q + e of
+//                           column 512 + c at [k][c][q][e] (quarter q of each block)
+//   alpha [alpha_ld]        softmax weights (unnormalised), written by wave 0; zero
+//                           past the current history
 //   sm    [4]               1 / softmax sum, STOP term of the older entries, newest weight
 //   hcol  [hcap]            history columns (START = n + 1)
 //   shist [hcap]            STOP column of the history B rows
@@ -168,8 +170,11 @@ __device__ __forceinline__ int key_index(uint64_t k) {
 // One workgroup runs one episode with W waves.  Thread j < 64 W owns
 // candidate column j: its history B values are in registers (the first RREG
 // entries), then in LDS (lt entries), then re-read from the Gram buffer.
-// With SEC (W = 8, 513-576 tokens) lane c of wave 0 also owns column 512 + c,
-// with its history in LDS.  STOP is not a column: its history term is a dot
+// With SEC (W = 8, 513-576 tokens) waves 0-3 (one per SIMD) also own the
+// columns 512-575: lane 4 c + q of wave w sums quarter q of every 16-entry
+// block of the history of column 512 + 16 w + c (history in LDS), and a quad
+// reduction combines the four quarters.  Each SIMD then carries the same
+// share of the step's FMAs.  STOP is not a column: its history term is a dot
 // product of the weights with the STOP column of the history rows, reduced
 // inside the softmax.
 //
@@ -227,8 +232,11 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   const float* CK = A + (int64_t)(2 * n + 2) * ld;           // the three parts of cK
   const int j = tid;
   const bool mcol = j < n;
-  const int js = 512 + lane;                                 // second column (wave 0)
-  const bool scol = SEC && wave == 0 && js < n;
+  const int sq = lane & 3;                                   // history quarter (second columns)
+  const int scl = (wave << 4) | (lane >> 2);                 // second column - 512
+  const int js = 512 + scl;
+  const bool swave = SEC && wave < 4;
+  const bool scol = swave && js < n;
   const float sigma = p.sigma, c1 = p.c1;
 
   auto ckv = [&](int c) { return (CK[c] + CK[ld + c]) + CK[2 * ld + c]; };
@@ -237,9 +245,13 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   const float ck_stop = ckv(n);
 
   for (int i = 0; i < lt; ++i) hmain[j * lt + i] = 0.0f;
-  if (SEC && wave == 0)
-    for (int i = 0; i < ks; i += 4)
-      *reinterpret_cast<float4*>(hsec + ((i >> 2) * 64 + lane) * 4) = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (SEC)
+    for (int i = tid; i < ks * 16; i += 64 * W)
+      reinterpret_cast<float4*>(hsec)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  // alpha past the history stays zero: wave 0 (its only writer) clears it
+  // before its first softmax.
+  if (wave == 0)
+    for (int i = lane; i < p.alpha_ld; i += 64) alpha[i] = 0.0f;
   if (tid < 2) key[tid] = 0ull;
 
   // Lane-owned history values in 32-wide vector registers.  Reads use
@@ -281,18 +293,24 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   auto softmax_w0 = [&](const float* Ar) {
     const int hpad = (hl + 15) & ~15;
     float m, sum = 0.0f, s2 = 0.0f;
+    // The newest entry's own score, requested with the gathers below.
+    const float r_new = Ar[ecol];
     if (hl <= 256) {
-      const float x0 = lane < hl ? Ar[hc0] * c1 : -INFINITY;
-      const float x1 = 64 < hl && lane + 64 < hl ? Ar[hc1] * c1 : -INFINITY;
-      const float x2 = 128 < hl && lane + 128 < hl ? Ar[hc2] * c1 : -INFINITY;
-      const float x3 = 192 < hl && lane + 192 < hl ? Ar[hc3] * c1 : -INFINITY;
+      // Every lane requests all four scores at once (columns without an entry
+      // hold a valid column), so the gathers share one memory round trip.
+      float r0 = Ar[hc0], r1 = Ar[hc1], r2 = Ar[hc2], r3 = Ar[hc3];
+      asm volatile("" : "+v"(r0), "+v"(r1), "+v"(r2), "+v"(r3));   // not sunk into branches
+      const float x0 = lane < hl ? r0 * c1 : -INFINITY;
+      const float x1 = lane + 64 < hl ? r1 * c1 : -INFINITY;
+      const float x2 = lane + 128 < hl ? r2 * c1 : -INFINITY;
+      const float x3 = lane + 192 < hl ? r3 * c1 : -INFINITY;
       m = wave_max_fused(fmaxf(fmaxf(x0, x1), fmaxf(x2, x3)));
       auto one = [&](int k, float x) {
         const int tau = lane + 64 * k;
         const float e = tau < hl ? __builtin_amdgcn_exp2f(x - m) : 0.0f;
         sum += e;
         s2 = fmaf(e, tau < hl - 1 ? shist[opaque(tau < hl - 1 ? tau : 0)] : 0.0f, s2);
-        if (tau < hpad) alpha[tau] = e;
+        if (tau < hpad) alpha[opaque(tau)] = e;
       };
       one(0, x0);
       if (64 < hpad) one(1, x1);
@@ -314,7 +332,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     if (lane == 0) {
       sm[0] = __builtin_amdgcn_rcpf(sum);
       sm[1] = s2;
-      sm[2] = __builtin_amdgcn_exp2f(Ar[ecol] * c1 - m);
+      sm[2] = __builtin_amdgcn_exp2f(r_new * c1 - m);
     }
   };
 
@@ -351,7 +369,8 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     const int pos = hl - 1;
     if (pos < RREG) hput(pos, b_main);
     else if (pos < RREG + lt) hmain[opaque(j) * lt + (pos - RREG)] = b_main;
-    if (SEC && wave == 0 && pos < ks) hsec[((pos >> 2) * 64 + opaque(lane)) * 4 + (pos & 3)] = b_sec;
+    if (swave && pos < ks && sq == ((pos >> 2) & 3))
+      hsec[(((pos >> 4) * 64 + opaque(scl)) * 4 + sq) * 4 + (pos & 3)] = b_sec;
     if (tid == 0) shist[pos] = b_stop;
   };
 
@@ -378,7 +397,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
         const int blk = bi * 16;
         if (blk < hl) {
           const int cur = bi & 1, nxt = cur ^ 1;
-          if (blk + 16 < RREG && blk + 16 < hl) {
+          if (blk + 16 < RREG) {   // unconditional: a uniform skip would make every wait conservative
             xa[nxt][0] = a4[(blk + 16) / 4 + 0];
             xa[nxt][1] = a4[(blk + 16) / 4 + 1];
             xa[nxt][2] = a4[(blk + 16) / 4 + 2];
@@ -442,19 +461,23 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     const float sp = fmaf(e_new, b_stop, st);
     const float l_stop = sigma * (ck_stop + a_stop + sp * inv) + p.b_stop;
 
-    // ---- wave 0's second columns: all their history in LDS (then global)
+    // ---- second columns (waves 0-3): each lane sums its quarter of every
+    // 16-entry block, 64 entries per pass with all eight reads issued first.
+    // Entries past the newest are zero in LDS and alpha is zero past the
+    // history, so whole passes need no masking.
     float ls = -INFINITY;
-    if (SEC && wave == 0) {
+    if (swave) {
       float acc2 = 0.0f, acc2b = 0.0f;
       const int last = hl - 1;                 // the newest entry is added below
       const int lend = last < ks ? last : ks;
-      int tau = 0;
-      for (; tau + 16 <= lend; tau += 16) {
+      const float* as = alpha + 4 * sq;
+      const float* hs = hsec + (opaque(scl) * 4 + sq) * 4;
+      for (int k0 = 0; 16 * k0 < lend; k0 += 4) {
         float4 av[4], hv[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          av[u] = *reinterpret_cast<const float4*>(alpha + tau + 4 * u);
-          hv[u] = *reinterpret_cast<const float4*>(hsec + (((tau >> 2) + u) * 64 + lane) * 4);
+          av[u] = *reinterpret_cast<const float4*>(as + 16 * (k0 + u));
+          hv[u] = *reinterpret_cast<const float4*>(hs + (k0 + u) * 1024);
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -464,33 +487,31 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
           acc2b = fmaf(av[u].w, hv[u].w, acc2b);
         }
       }
-      for (; tau < lend; tau += 4) {
-        // entries past `last` in this block are zero in LDS and in alpha's padding
-        const float4 av = *reinterpret_cast<const float4*>(alpha + tau);
-        const float4 hv = *reinterpret_cast<const float4*>(hsec + ((tau >> 2) * 64 + lane) * 4);
-        acc2 = fmaf(av.x, hv.x, acc2);
-        acc2b = fmaf(av.y, hv.y, acc2b);
-        acc2 = fmaf(av.z, hv.z, acc2);
-        acc2b = fmaf(av.w, hv.w, acc2b);
-      }
-      for (tau = ks; tau < last; ++tau) {
+      // entries past the LDS tier: read again from the Gram buffer, every
+      // fourth one per lane
+      for (int tau = ks + sq; tau < last; tau += 4) {
         const int c = hcol[tau];
         const float hv = scol ? Bm[(int64_t)(c == n + 1 ? n : c) * ld + js] : 0.0f;
         acc2 = fmaf(alpha[tau], hv, acc2);
       }
-      acc2 = fmaf(e_new, b_sec, acc2 + acc2b);
-      ls = scol && !sel_sec ? sigma * (ck_sec + a_sec + acc2 * inv) : -INFINITY;
+      // quad sum of the four quarters: (q0 + q1) + (q2 + q3) in every lane of
+      // the quad (each addition is commutative, so all four agree bit for bit)
+      float qs = acc2 + acc2b;
+      qs += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(qs), 0xB1, 0xF, 0xF, true));
+      qs += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(qs), 0x4E, 0xF, 0xF, true));
+      qs = fmaf(e_new, b_sec, qs);
+      ls = scol && !sel_sec ? sigma * (ck_sec + a_sec + qs * inv) : -INFINITY;
     }
 
     // ---- this wave's best candidate (lowest index on ties) into the key
     const bool valid = mcol && !selected;
     const float v = valid ? lj : -INFINITY;
-    const float vmax = wave_max_fused(SEC ? fmaxf(v, ls) : v);
+    const float vmax = wave_max_fused(swave ? fmaxf(v, ls) : v);
     int i1 = -1;
     if (vmax > -INFINITY) {
       const uint64_t m1 = __ballot(valid && v == vmax);
       if (m1) i1 = wave * 64 + __ffsll((unsigned long long)m1) - 1;
-      else if (SEC) i1 = 512 + __ffsll((unsigned long long)__ballot(ls == vmax)) - 1;
+      else if (SEC) i1 = 512 + (wave << 4) + ((__ffsll((unsigned long long)__ballot(ls == vmax)) - 1) >> 2);
       if (lane == 0) atomicMax(&key[par], (unsigned long long)cand_key(vmax, i1));
     }
     if (tid == 0 && l_stop > -INFINITY) atomicMax(&key[par], (unsigned long long)cand_key(l_stop, n));
@@ -532,26 +553,30 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   }
 
   // ---- native order (Algorithm 1 step 4): ascending positions of the set
-  // bits, lane-owned columns first, then wave 0's second columns.
+  // bits, lane-owned columns first, then the second columns (one lane of each
+  // quad reports; waves 0-3 hold them in ascending order).
   __syncthreads();
   const uint64_t ballot = __ballot(mcol && selected);
-  if (lane == 0) cnt[wave] = __popcll(ballot);
+  const uint64_t sb = __ballot(scol && sel_sec && sq == 0);
+  if (lane == 0) {
+    cnt[wave] = __popcll(ballot);
+    if (SEC && wave < 4) cnt[8 + wave] = __popcll(sb);
+  }
   __syncthreads();
-  int before = 0, total = 0;
+  int before = 0, total = 0, before2 = 0;
   for (int w = 0; w < W; ++w) {
     if (w < wave) before += cnt[w];
     total += cnt[w];
   }
+  if (SEC)
+    for (int w = 0; w < wave && w < 4; ++w) before2 += cnt[8 + w];
   if (mcol && selected) {
     const int pos = before + __popcll(ballot & ((1ull << lane) - 1ull));
     p.grp_kept[(int64_t)g * p.max_cap + pos] = j;
   }
-  if (SEC && wave == 0) {
-    const uint64_t sb = __ballot(scol && sel_sec);
-    if (scol && sel_sec) {
-      const int pos = total + __popcll(sb & ((1ull << lane) - 1ull));
-      p.grp_kept[(int64_t)g * p.max_cap + pos] = js;
-    }
+  if (scol && sel_sec && sq == 0) {
+    const int pos = total + before2 + __popcll(sb & ((1ull << lane) - 1ull));
+    p.grp_kept[(int64_t)g * p.max_cap + pos] = js;
   }
   if (tid == 0) {
     p.grp_count[g] = kept;
@@ -685,7 +710,9 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   int rreg = wide ? 32 : need <= 64 ? 64 : need <= 128 ? 128 : 160;
   p.W = W;
   p.hcap = (int)align_up((size_t)need + 1, 4);
-  p.alpha_ld = (int)align_up((size_t)need, 16);
+  // alpha covers the register blocks' prefetch (up to rreg) and the second
+  // columns' 64-entry passes.
+  p.alpha_ld = (int)align_up((size_t)(need > rreg ? need : rreg), sec ? 64 : 16);
   p.sigma = 1.0f / sqrtf((float)a.h);
   p.c1 = p.sigma * 1.4426950408889634f;
   // LDS: fixed arrays, then wave 0's second-column history (all of it if it
@@ -695,9 +722,9 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   size_t room = fixed < (size_t)kLdsBytes ? (size_t)kLdsBytes - fixed : 0;
   int ks = 0;
   if (sec) {
-    ks = (need + 3) / 4 * 4;
+    ks = (need + 63) / 64 * 64;                         // whole 64-entry passes
     const size_t per = 64 * 4;
-    if ((size_t)ks * per > room) ks = (int)(room / per) / 4 * 4;
+    if ((size_t)ks * per > room) ks = (int)(room / per) / 64 * 64;
     room -= (size_t)ks * per;
   }
   int lt = 0;
