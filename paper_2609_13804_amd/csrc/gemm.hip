@@ -180,22 +180,22 @@ __device__ __forceinline__ void gemm_block(const ARows& ar, const BRows& br, int
 
 // ------------------------------------------------------------------ bf16, 256 x 256 tiles
 //
-// Large bfloat16 GEMMs: a 256 x 256 output tile per workgroup of four waves
-// (each wave 128 x 128 = 4 x 4 MFMA 32x32x16 tiles, accumulators in AGPRs),
-// K in 32-wide stages.  Operand tiles go straight from global memory into LDS
+// Large bfloat16 GEMMs: a 256 x 256 output tile per workgroup of four or
+// eight waves (MFMA 32x32x16 tiles, accumulators in AGPRs), K in 32-wide
+// stages.  Operand tiles go straight from global memory into LDS
 // (global_load_lds_dwordx4: one wave instruction fills 1 KiB = 16 rows x 64
 // bytes) through a ring of S stage buffers, loads running S - 1 stages ahead
-// of the matrix cores.  Within a 64-byte row the four 16-byte chunks are
-// stored XOR-swizzled (chunk c of row r at slot c ^ ((r >> 2) & 3)), which the
-// load realises by choosing each lane's source address: a 16-byte fragment
-// read serves 16 lanes (16 consecutive rows, 4 rows per 256-byte pass over the
-// 64 banks) at a time, and rows 4 apart take different slots, so no two lanes
-// of a pass share a bank.  Rows past M (N) are
-// clamped to the last valid row and their results are not stored.
+// of the matrix cores.  Each stage's loads are issued a few at a time between
+// matrix-core instructions rather than in one burst.  Within a 64-byte row
+// the four 16-byte chunks are stored XOR-swizzled (chunk c of row r at slot
+// c ^ ((r >> 2) & 3)), which the load realises by choosing each lane's source
+// address: a 16-byte fragment read serves 16 lanes (16 consecutive rows, 4 rows
+// per 256-byte pass over the 64 banks) at a time, and rows 4 apart take
+// different slots, so no two lanes of a pass share a bank.  Rows past M (N)
+// are clamped to the last valid row and their results are not stored.
 constexpr int kBM = 256, kBN = 256, kBK = 32, kStages = 4;
 constexpr int kOpBytes = kBM * kBK * 2;                // one operand tile, 16 KiB
 constexpr int kStageBytes = 2 * kOpBytes;              // A and B, 32 KiB
-constexpr int kLoadsPerWave = 2 * kOpBytes / 1024 / 4; // DMA instructions per wave per stage
 
 typedef __attribute__((address_space(1))) const void* gptr_t;
 typedef __attribute__((address_space(3))) void* lptr_t;
@@ -216,25 +216,33 @@ __device__ __forceinline__ int swz(int row, int chunk) {
   return row * 64 + ((chunk ^ ((row >> 2) & 3)) << 4);
 }
 
-template <typename OutT, class ARows, class BRows>
+// WAVES = 4: each wave owns a 128 x 128 quadrant (one wave per SIMD).
+// WAVES = 8: each wave owns 128 x 64 (two waves per SIMD, so one wave's
+// matrix-core work covers the other's waits at barriers and loads).
+template <int WAVES, typename OutT, class ARows, class BRows>
 __device__ __forceinline__ void gemm_bf16_256(const ARows& ar, const BRows& br, int64_t M,
                                               int64_t N, int K, OutT* __restrict__ C, int64_t ldc,
                                               int64_t m0, int64_t n0, char* smem) {
+  static_assert(WAVES == 4 || WAVES == 8, "four or eight waves");
+  constexpr int GPW = 16 / WAVES;            // 16-row groups per operand per wave
+  constexpr int LPW = 2 * GPW;               // DMA instructions per wave per stage
+  constexpr int WGN = WAVES / 2;             // waves along N (two along M)
+  constexpr int TN = 8 / WGN;                // 32-column MFMA tiles per wave along N
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
 
-  // This wave loads 16-row groups wave + 4 i (i < 4) of both operand tiles;
-  // lane (rl = lane / 4, slot = lane % 4) fetches chunk slot ^ ((rl >> 2) & 3)
-  // of row rl.
+  // This wave loads 16-row groups wave + WAVES i (i < GPW) of both operand
+  // tiles; lane (rl = lane / 4, slot = lane % 4) fetches chunk
+  // slot ^ ((rl >> 2) & 3) of row rl.
   const int rl = lane >> 2;
   const int chunk = (lane & 3) ^ ((rl >> 2) & 3);
-  const __bf16* pa[4];
-  const __bf16* pb[4];
+  const __bf16* pa[GPW];
+  const __bf16* pb[GPW];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = 16 * (wave + 4 * i) + rl;
+  for (int i = 0; i < GPW; ++i) {
+    const int r = 16 * (wave + WAVES * i) + rl;
     const int64_t gm = m0 + r < M ? m0 + r : M - 1;
     const int64_t gn = n0 + r < N ? n0 + r : N - 1;
     pa[i] = ar.row(gm) + chunk * 8;
@@ -244,28 +252,28 @@ __device__ __forceinline__ void gemm_bf16_256(const ARows& ar, const BRows& br, 
     char* a = smem + buf * kStageBytes;
     char* b = a + kOpBytes;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) lds_dma16(pa[i] + k0, a + (wave + 4 * i) * 1024);
+    for (int i = 0; i < GPW; ++i) lds_dma16(pa[i] + k0, a + (wave + WAVES * i) * 1024);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) lds_dma16(pb[i] + k0, b + (wave + 4 * i) * 1024);
+    for (int i = 0; i < GPW; ++i) lds_dma16(pb[i] + k0, b + (wave + WAVES * i) * 1024);
   };
 
-  f32x16_t acc[4][4];
+  f32x16_t acc[4][TN];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const int arow0 = wm * 128 + (lane & 31);
-  const int brow0 = wn * 128 + (lane & 31);
+  const int brow0 = wn * (32 * TN) + (lane & 31);
   const int khalf = lane >> 5;
-  auto load_frags = [&](const char* As, const char* Bs, int ks, bf16x8_t (&a)[4], bf16x8_t (&b)[4]) {
+  auto load_frags = [&](const char* As, const char* Bs, int ks, bf16x8_t (&a)[4], bf16x8_t (&b)[TN]) {
     const int c = ks * 2 + khalf;
 #pragma unroll
     for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const bf16x8_t*>(As + swz(arow0 + 32 * i, c));
 #pragma unroll
-    for (int j = 0; j < 4; ++j) b[j] = *reinterpret_cast<const bf16x8_t*>(Bs + swz(brow0 + 32 * j, c));
+    for (int j = 0; j < TN; ++j) b[j] = *reinterpret_cast<const bf16x8_t*>(Bs + swz(brow0 + 32 * j, c));
   };
 
   // Software pipeline over K stages.  Iteration kt multiplies stage kt in two
@@ -277,62 +285,81 @@ __device__ __forceinline__ void gemm_bf16_256(const ARows& ar, const BRows& br, 
 #pragma unroll
   for (int s = 0; s < kStages - 1; ++s)
     if (s < KT) issue(s, s * kBK);
-  if (KT > kStages - 2) wait_vmcnt<(kStages - 2) * kLoadsPerWave>();
+  if (KT > kStages - 2) wait_vmcnt<(kStages - 2) * LPW>();
   else wait_vmcnt<0>();
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
-  bf16x8_t a0[4], b0[4], a1[4], b1[4];
-  load_frags(smem, smem + kOpBytes, 0, a0, b0);
-  load_frags(smem, smem + kOpBytes, 1, a1, b1);
-  for (int kt = 0; kt < KT; ++kt) {
+  // Two fragment sets used in turn (the loop is unrolled by two), so the
+  // next stage's fragments land in registers no copy has to wait for.
+  struct Frags {
+    bf16x8_t a0[4], b0[TN], a1[4], b1[TN];
+  };
+  Frags f0, f1;
+  load_frags(smem, smem + kOpBytes, 0, f0.a0, f0.b0);
+  load_frags(smem, smem + kOpBytes, 1, f0.a1, f0.b1);
+  // DMA instruction q of a stage: the first GPW fill A's row groups, the rest B's.
+  auto issue_one = [&](int buf, int k0, int q) {
+    char* a = smem + buf * kStageBytes;
+    if (q < GPW) lds_dma16(pa[q] + k0, a + (wave + WAVES * q) * 1024);
+    else lds_dma16(pb[q - GPW] + k0, a + kOpBytes + (wave + WAVES * (q - GPW)) * 1024);
+  };
+  auto step = [&](int kt, Frags& cur, Frags& nxt) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[i], b0[j], acc[i][j], 0, 0, 0);
-    bf16x8_t na0[4], nb0[4], na1[4], nb1[4];
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a0[i], cur.b0[j], acc[i][j], 0, 0, 0);
     const bool more = kt + 1 < KT;
+    const bool refill = kt + kStages - 1 < KT;
     if (more) {
       // Stage kt + 1 has landed once at most (stages issued after it) x loads
-      // of this wave remain; all fragment reads of stage kt are complete.
-      if (kt + kStages - 1 < KT) wait_vmcnt<(kStages - 3) * kLoadsPerWave>();
+      // of this wave remain.  The buffer refilled below held stage kt - 1,
+      // whose fragments every wave consumed before this barrier.
+      if (refill) wait_vmcnt<(kStages - 3) * LPW>();
       else wait_vmcnt<0>();
-      __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
       // Bare s_barrier (no fence): a workgroup fence would wait for every load
       // still in flight and collapse the ring to a single stage.
       __builtin_amdgcn_s_barrier();
       asm volatile("" ::: "memory");
-      if (kt + kStages - 1 < KT) issue((kt + kStages - 1) % kStages, (kt + kStages - 1) * kBK);
       const char* As = smem + ((kt + 1) % kStages) * kStageBytes;
-      load_frags(As, As + kOpBytes, 0, na0, nb0);
+      load_frags(As, As + kOpBytes, 0, nxt.a0, nxt.b0);
     }
     __builtin_amdgcn_sched_barrier(0);
+    // The refill of stage kt + S - 1 is spread over this half's matrix-core
+    // work: issued in one burst, the loads would stall this wave's issue until
+    // the memory pipeline drained them, and the matrix cores with it.
+    const int rbuf = (kt + kStages - 1) % kStages, rk0 = (kt + kStages - 1) * kBK;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b1[j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a1[i], cur.b1[j], acc[i][j], 0, 0, 0);
+      if (refill) {
+#pragma unroll
+        for (int u = 0; u < LPW / 4; ++u) issue_one(rbuf, rk0, i * (LPW / 4) + u);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
     if (more) {
       const char* As = smem + ((kt + 1) % kStages) * kStageBytes;
-      load_frags(As, As + kOpBytes, 1, na1, nb1);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        a0[i] = na0[i];
-        b0[i] = nb0[i];
-        a1[i] = na1[i];
-        b1[i] = nb1[i];
-      }
+      load_frags(As, As + kOpBytes, 1, nxt.a1, nxt.b1);
     }
     __builtin_amdgcn_sched_barrier(0);
+  };
+  int kt = 0;
+  for (; kt + 1 < KT; kt += 2) {
+    step(kt, f0, f1);
+    step(kt + 1, f1, f0);
   }
+  if (kt < KT) step(kt, f0, f1);
 
   // 32x32 MFMA result layout: lane l, register r holds
   // row 8*(r/4) + 4*(l/32) + r%4, column l%32.
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t col = n0 + wn * 128 + j * 32 + (lane & 31);
+    for (int j = 0; j < TN; ++j) {
+      const int64_t col = n0 + wn * (32 * TN) + j * 32 + (lane & 31);
       if (col >= N) continue;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -417,16 +444,18 @@ __global__ __launch_bounds__(kThreads) void project_gemm_kernel(ProjRows<T> ar, 
   gemm_block<T, OutT, BM, BN, BK>(ar, br, M, N, K, C, N, (t / nt) * BM, (t % nt) * BN, smem);
 }
 
-__global__ __launch_bounds__(kThreads) void project_gemm_bf16_kernel(ProjRows<__bf16> ar,
-                                                                    DenseRows<__bf16> br,
-                                                                    int64_t M, int64_t N, int K,
-                                                                    uint16_t* C) {
+constexpr int kProjWaves = 8;
+
+__global__ __launch_bounds__(64 * kProjWaves) void project_gemm_bf16_kernel(ProjRows<__bf16> ar,
+                                                                          DenseRows<__bf16> br,
+                                                                          int64_t M, int64_t N,
+                                                                          int K, uint16_t* C) {
   __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes];
   const int64_t nt = (N + kBN - 1) / kBN;
   const int64_t tiles = ((M + kBM - 1) / kBM) * nt;
   const int64_t t = xcd_tile(blockIdx.x, tiles);
   if (t < 0) return;
-  gemm_bf16_256<uint16_t>(ar, br, M, N, K, C, N, (t / nt) * kBM, (t % nt) * kBN, smem);
+  gemm_bf16_256<kProjWaves, uint16_t>(ar, br, M, N, K, C, N, (t / nt) * kBM, (t % nt) * kBN, smem);
 }
 
 // grid.x: output tiles, grid.y: K split p, which covers k in [p K, (p + 1) K)
@@ -504,7 +533,9 @@ __device__ __forceinline__ bool gram_group_ok(const GramArgs& a, int64_t g, int6
 
 // bfloat16 Gram products on the 256 x 256 direct-to-LDS core: 15 tiles per
 // 576-token group, one round for 16 groups.
-__global__ __launch_bounds__(kThreads) void gram_gemm_bf16_kernel(GramArgs a, int per_group,
+constexpr int kGramWaves = 4;
+
+__global__ __launch_bounds__(64 * kGramWaves) void gram_gemm_bf16_kernel(GramArgs a, int per_group,
                                                                  int xcd_grouped) {
   __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes];
   int64_t g, t, g0, n;
@@ -519,7 +550,7 @@ __global__ __launch_bounds__(kThreads) void gram_gemm_bf16_kernel(GramArgs a, in
   if (m0 >= M || n0 >= N) return;   // tile outside this (smaller) group
   GramARows<__bf16> ar{KQV, g0, n, a.T_vis, a.h, cs};
   GramBRows<__bf16> br{KQV, g0, n, a.T_vis, a.h};
-  gemm_bf16_256<float>(ar, br, M, N, a.h, a.gram + g * a.gram_group_stride, a.gram_ld, m0, n0,
+  gemm_bf16_256<kGramWaves, float>(ar, br, M, N, a.h, a.gram + g * a.gram_group_stride, a.gram_ld, m0, n0,
                        smem);
 }
 
@@ -557,7 +588,7 @@ hipError_t launch_project_gemm(int dtype, const void* X, int64_t T_vis, const vo
     DenseRows<__bf16> br{(const __bf16*)W, d};
     const int64_t tiles = ceil_div(M, kBM) * ceil_div(N, kBN);
     hipLaunchKernelGGL(project_gemm_bf16_kernel, dim3((unsigned)(ceil_div(tiles, 8) * 8)),
-                       dim3(kThreads), 0, stream, ar, br, M, N, d, (uint16_t*)out);
+                       dim3(64 * kProjWaves), 0, stream, ar, br, M, N, d, (uint16_t*)out);
   } else {
     constexpr int BM = 128, BN = 128, BK = 32;
     ProjRows<float> ar{(const float*)X, T_vis, (const float*)s_start, (const float*)s_stop, d};
@@ -608,7 +639,7 @@ hipError_t launch_gram_gemm(const GramArgs& a, hipStream_t stream) {
     const int per_group = (int)(ceil_div(M, kBM) * ceil_div(N, kBN));
     const int64_t blocks =
         xcd_grouped ? 8 * ceil_div(a.G, 8) * per_group : (int64_t)a.G * per_group;
-    hipLaunchKernelGGL(gram_gemm_bf16_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, a,
+    hipLaunchKernelGGL(gram_gemm_bf16_kernel, dim3((unsigned)blocks), dim3(64 * kGramWaves), 0, stream, a,
                        per_group, xcd_grouped);
   } else {
     hipLaunchKernelGGL(ctx_split_kernel<float>, dim3(a.B), dim3(256), 0, stream, a.ctx, a.h,
