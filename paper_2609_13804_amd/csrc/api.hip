@@ -49,7 +49,7 @@ SelectWs select_ws_layout(const sp_dims* d, int B, int G, int max_group, int max
 
 // Header, then the text projection's K-split partial products [split][T_txt][h].
 size_t project_ws_bytes(const sp_dims* d, int64_t T_txt) {
-  const size_t split = (size_t)text_split(T_txt, d->h, d->d_text);
+  const size_t split = (size_t)text_split(d->dtype, T_txt, d->h, d->d_text);
   return kWsHeaderBytes + align_up(split * (size_t)T_txt * d->h * 4, 256);
 }
 
@@ -105,13 +105,12 @@ sp_status stepprune_project(const sp_dims* dims, const void* X, int64_t T_vis, c
   float* tproj = reinterpret_cast<float*>(static_cast<char*>(ws) + kWsHeaderBytes);
   record_event(events, 0, stream);
   hipError_t e = launch_project_gemm(dims->dtype, X, T_vis, s_start, s_stop, W_kqv, dims->d,
-                                     3 * dims->h, KQV, stream);
+                                     3 * dims->h, KQV, E_text, T_txt, W_text, dims->d_text,
+                                     dims->h, tproj, stream);
   record_event(events, 1, stream);
   if (e == hipSuccess)
-    e = launch_text_gemm(dims->dtype, E_text, T_txt, W_text, dims->d_text, dims->h, tproj, stream);
-  if (e == hipSuccess)
-    e = launch_text_pool(tproj, text_split(T_txt, dims->h, dims->d_text), text_off, B, T_txt,
-                         dims->h, g_text, ln_eps, ctx, err, stream);
+    e = launch_text_pool(tproj, text_split(dims->dtype, T_txt, dims->h, dims->d_text), text_off, B,
+                         T_txt, dims->h, g_text, ln_eps, ctx, err, stream);
   return hip_status(e);
 }
 

@@ -446,16 +446,27 @@ __global__ __launch_bounds__(kThreads) void project_gemm_kernel(ProjRows<T> ar, 
 
 constexpr int kProjWaves = 8;
 
-__global__ __launch_bounds__(64 * kProjWaves) void project_gemm_bf16_kernel(ProjRows<__bf16> ar,
-                                                                          DenseRows<__bf16> br,
-                                                                          int64_t M, int64_t N,
-                                                                          int K, uint16_t* C) {
+// Blocks [0, proj_blocks) take the projection's tiles in XCD-grouped order
+// (bfloat16 output); the blocks after them take the text projection's tiles
+// (float32 output).  The text tiles are dispatched last, onto the compute
+// units the projection's last round leaves idle.
+__global__ __launch_bounds__(64 * kProjWaves) void project_gemm_bf16_kernel(
+    ProjRows<__bf16> ar, DenseRows<__bf16> br, int64_t M, int64_t N, int K, uint16_t* C,
+    int64_t proj_blocks, DenseRows<__bf16> er, DenseRows<__bf16> wr, int64_t M2, int64_t N2, int K2,
+    float* C2) {
   __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes];
-  const int64_t nt = (N + kBN - 1) / kBN;
-  const int64_t tiles = ((M + kBM - 1) / kBM) * nt;
-  const int64_t t = xcd_tile(blockIdx.x, tiles);
-  if (t < 0) return;
-  gemm_bf16_256<kProjWaves, uint16_t>(ar, br, M, N, K, C, N, (t / nt) * kBM, (t % nt) * kBN, smem);
+  if ((int64_t)blockIdx.x < proj_blocks) {
+    const int64_t nt = (N + kBN - 1) / kBN;
+    const int64_t tiles = ((M + kBM - 1) / kBM) * nt;
+    const int64_t t = xcd_tile(blockIdx.x, tiles);
+    if (t < 0) return;
+    gemm_bf16_256<kProjWaves, uint16_t>(ar, br, M, N, K, C, N, (t / nt) * kBM, (t % nt) * kBN, smem);
+  } else {
+    const int64_t nt = (N2 + kBN - 1) / kBN;
+    const int64_t t = (int64_t)blockIdx.x - proj_blocks;
+    gemm_bf16_256<kProjWaves, float>(er, wr, M2, N2, K2, C2, N2, (t / nt) * kBM, (t % nt) * kBN,
+                                     smem);
+  }
 }
 
 // grid.x: output tiles, grid.y: K split p, which covers k in [p K, (p + 1) K)
@@ -579,28 +590,8 @@ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 }  // namespace
 
-hipError_t launch_project_gemm(int dtype, const void* X, int64_t T_vis, const void* s_start,
-                               const void* s_stop, const void* W, int d, int n_out, void* out,
-                               hipStream_t stream) {
-  const int64_t M = T_vis + 2, N = n_out;
-  if (dtype == SP_BF16) {
-    ProjRows<__bf16> ar{(const __bf16*)X, T_vis, (const __bf16*)s_start, (const __bf16*)s_stop, d};
-    DenseRows<__bf16> br{(const __bf16*)W, d};
-    const int64_t tiles = ceil_div(M, kBM) * ceil_div(N, kBN);
-    hipLaunchKernelGGL(project_gemm_bf16_kernel, dim3((unsigned)(ceil_div(tiles, 8) * 8)),
-                       dim3(64 * kProjWaves), 0, stream, ar, br, M, N, d, (uint16_t*)out);
-  } else {
-    constexpr int BM = 128, BN = 128, BK = 32;
-    ProjRows<float> ar{(const float*)X, T_vis, (const float*)s_start, (const float*)s_stop, d};
-    DenseRows<float> br{(const float*)W, d};
-    hipLaunchKernelGGL((project_gemm_kernel<float, float, BM, BN, BK>),
-                       dim3((unsigned)(ceil_div(M, BM) * ceil_div(N, BN))), dim3(kThreads), 0, stream,
-                       ar, br, M, N, d, (float*)out);
-  }
-  return hipGetLastError();
-}
-
-int text_split(int64_t T_txt, int h, int d_text) {
+int text_split(int dtype, int64_t T_txt, int h, int d_text) {
+  if (dtype == SP_BF16) return 1;   // computed beside the projection, whole K
   // Enough workgroups to cover the chip: split K while the tiles are fewer
   // than 512, up to 8 ways, keeping each part a whole number of 64-wide stages.
   const int64_t tiles = ceil_div(T_txt, 128) * ceil_div(h, 128);
@@ -609,24 +600,49 @@ int text_split(int64_t T_txt, int h, int d_text) {
   return s;
 }
 
-hipError_t launch_text_gemm(int dtype, const void* E, int64_t T_txt, const void* W, int d_text,
-                            int h, float* out, hipStream_t stream) {
+namespace {
+
+hipError_t launch_text_gemm_f32(const void* E, int64_t T_txt, const void* W, int d_text, int h,
+                                float* out, hipStream_t stream) {
   if (T_txt == 0) return hipSuccess;
-  const int split = text_split(T_txt, h, d_text);
+  const int split = text_split(SP_F32, T_txt, h, d_text);
   const int kpart = d_text / split;
   const dim3 grid((unsigned)(ceil_div(T_txt, 128) * ceil_div(h, 128)), (unsigned)split);
-  if (dtype == SP_BF16) {
-    DenseRows<__bf16> ar{(const __bf16*)E, d_text};
-    DenseRows<__bf16> br{(const __bf16*)W, d_text};
-    hipLaunchKernelGGL((dense_gemm_kernel<__bf16, 128, 128, 64>), grid, dim3(kThreads), 0, stream,
-                       ar, br, T_txt, (int64_t)h, kpart, out);
-  } else {
-    DenseRows<float> ar{(const float*)E, d_text};
-    DenseRows<float> br{(const float*)W, d_text};
-    hipLaunchKernelGGL((dense_gemm_kernel<float, 128, 128, 32>), grid, dim3(kThreads), 0, stream,
-                       ar, br, T_txt, (int64_t)h, kpart, out);
-  }
+  DenseRows<float> ar{(const float*)E, d_text};
+  DenseRows<float> br{(const float*)W, d_text};
+  hipLaunchKernelGGL((dense_gemm_kernel<float, 128, 128, 32>), grid, dim3(kThreads), 0, stream,
+                     ar, br, T_txt, (int64_t)h, kpart, out);
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_project_gemm(int dtype, const void* X, int64_t T_vis, const void* s_start,
+                               const void* s_stop, const void* W, int d, int n_out, void* out,
+                               const void* E, int64_t T_txt, const void* W_text, int d_text, int h,
+                               float* tproj, hipStream_t stream) {
+  const int64_t M = T_vis + 2, N = n_out;
+  if (dtype == SP_BF16) {
+    ProjRows<__bf16> ar{(const __bf16*)X, T_vis, (const __bf16*)s_start, (const __bf16*)s_stop, d};
+    DenseRows<__bf16> br{(const __bf16*)W, d};
+    DenseRows<__bf16> er{(const __bf16*)E, d_text};
+    DenseRows<__bf16> wr{(const __bf16*)W_text, d_text};
+    const int64_t proj_blocks = ceil_div(ceil_div(M, kBM) * ceil_div(N, kBN), 8) * 8;
+    const int64_t text_blocks = T_txt > 0 ? ceil_div(T_txt, kBM) * ceil_div(h, kBN) : 0;
+    hipLaunchKernelGGL(project_gemm_bf16_kernel, dim3((unsigned)(proj_blocks + text_blocks)),
+                       dim3(64 * kProjWaves), 0, stream, ar, br, M, N, d, (uint16_t*)out,
+                       proj_blocks, er, wr, T_txt, (int64_t)h, d_text, tproj);
+    return hipGetLastError();
+  }
+  constexpr int BM = 128, BN = 128, BK = 32;
+  ProjRows<float> ar{(const float*)X, T_vis, (const float*)s_start, (const float*)s_stop, d};
+  DenseRows<float> br{(const float*)W, d};
+  hipLaunchKernelGGL((project_gemm_kernel<float, float, BM, BN, BK>),
+                     dim3((unsigned)(ceil_div(M, BM) * ceil_div(N, BN))), dim3(kThreads), 0, stream,
+                     ar, br, M, N, d, (float*)out);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_text_gemm_f32(E, T_txt, W_text, d_text, h, tproj, stream);
 }
 
 hipError_t launch_gram_gemm(const GramArgs& a, hipStream_t stream) {

@@ -277,6 +277,9 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   };
   // History column of entry lane + 64 k, for the first 256 entries.
   int hc0 = 0, hc1 = 0, hc2 = 0, hc3 = 0;
+  // Wave 0: the STOP column of the history's B rows, entry lane + 64 k in
+  // slot k (also kept in LDS for histories past 256 entries).
+  float sh0 = 0.0f, sh1 = 0.0f, sh2 = 0.0f, sh3 = 0.0f;
 
   // The newest history entry (position hl - 1): its column, its A values, and
   // its B values, which are stored into the history one step later.
@@ -305,17 +308,17 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
       const float x2 = lane + 128 < hl ? r2 * c1 : -INFINITY;
       const float x3 = lane + 192 < hl ? r3 * c1 : -INFINITY;
       m = wave_max_fused(fmaxf(fmaxf(x0, x1), fmaxf(x2, x3)));
-      auto one = [&](int k, float x) {
+      auto one = [&](int k, float x, float sh) {
         const int tau = lane + 64 * k;
         const float e = tau < hl ? __builtin_amdgcn_exp2f(x - m) : 0.0f;
         sum += e;
-        s2 = fmaf(e, tau < hl - 1 ? shist[opaque(tau < hl - 1 ? tau : 0)] : 0.0f, s2);
+        s2 = fmaf(e, tau < hl - 1 ? sh : 0.0f, s2);
         if (tau < hpad) alpha[opaque(tau)] = e;
       };
-      one(0, x0);
-      if (64 < hpad) one(1, x1);
-      if (128 < hpad) one(2, x2);
-      if (192 < hpad) one(3, x3);
+      one(0, x0, sh0);
+      if (64 < hpad) one(1, x1, sh1);
+      if (128 < hpad) one(2, x2, sh2);
+      if (192 < hpad) one(3, x3, sh3);
     } else {
       // longer histories: the scores are gathered again in each pass
       m = -INFINITY;
@@ -369,9 +372,18 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     const int pos = hl - 1;
     if (pos < RREG) hput(pos, b_main);
     else if (pos < RREG + lt) hmain[opaque(j) * lt + (pos - RREG)] = b_main;
+    // waves 0-3: 4 scl + sq is the thread index
     if (swave && pos < ks && sq == ((pos >> 2) & 3))
-      hsec[(((pos >> 4) * 64 + opaque(scl)) * 4 + sq) * 4 + (pos & 3)] = b_sec;
+      hsec[(((pos >> 4) * 256 + opaque(tid)) << 2) + (pos & 3)] = b_sec;
     if (tid == 0) shist[pos] = b_stop;
+    if (wave == 0) {
+      const int k = pos >> 6;
+      const bool mine = lane == (pos & 63);
+      if (__builtin_amdgcn_readfirstlane(k == 0) && mine) sh0 = b_stop;
+      if (__builtin_amdgcn_readfirstlane(k == 1) && mine) sh1 = b_stop;
+      if (__builtin_amdgcn_readfirstlane(k == 2) && mine) sh2 = b_stop;
+      if (__builtin_amdgcn_readfirstlane(k == 3) && mine) sh3 = b_stop;
+    }
   };
 
   load_entry(n, n + 1);   // history entry 0 is START: row n of A and B, column n + 1
@@ -470,8 +482,9 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
       float acc2 = 0.0f, acc2b = 0.0f;
       const int last = hl - 1;                 // the newest entry is added below
       const int lend = last < ks ? last : ks;
-      const float* as = alpha + 4 * sq;
-      const float* hs = hsec + (opaque(scl) * 4 + sq) * 4;
+      const int st4 = opaque(tid);                 // 4 scl + sq in waves 0-3
+      const float* as = alpha + 4 * (st4 & 3);
+      const float* hs = hsec + st4 * 4;
       for (int k0 = 0; 16 * k0 < lend; k0 += 4) {
         float4 av[4], hv[4];
 #pragma unroll

@@ -37,16 +37,18 @@ __device__ inline void set_device_error(int32_t* err, int32_t code) {
 // ---------------------------------------------------------------- GEMM launchers
 // C[m, n] = sum_k A[m, k] * B[n, k]  (both operands K-contiguous), fp32 accumulate.
 
-// Projection: A rows are X rows 0..T_vis-1, then s_start, then s_stop.
+// Projection: A rows are X rows 0..T_vis-1, then s_start, then s_stop; and
+// the text projection: A = E_text [T_txt, d_text], B = W_text [h, d_text],
+// float32 output split over K into text_split() partial products
+// [split][T_txt][h], which launch_text_pool adds in a fixed order.  For
+// bfloat16 both products run in one launch (the text tiles fill the compute
+// units the projection's last round leaves idle) and the text product is not
+// split.
+int text_split(int dtype, int64_t T_txt, int h, int d_text);
 hipError_t launch_project_gemm(int dtype, const void* X, int64_t T_vis, const void* s_start,
                                const void* s_stop, const void* W, int d, int n_out, void* out,
-                               hipStream_t stream);
-// Text projection: A = E_text [T_txt, d_text], B = W_text [h, d_text], fp32
-// output split over K into text_split() partial products [split][T_txt][h],
-// which launch_text_pool adds in a fixed order.
-int text_split(int64_t T_txt, int h, int d_text);
-hipError_t launch_text_gemm(int dtype, const void* E, int64_t T_txt, const void* W, int d_text,
-                            int h, float* out, hipStream_t stream);
+                               const void* E, int64_t T_txt, const void* W_text, int d_text, int h,
+                               float* tproj, hipStream_t stream);
 // Per-group Gram products of the projected rows (see select.hip for the
 // layout).  The text context of each image is first written as three rows of
 // the working dtype whose sum is exactly the float32 context (csplit,
