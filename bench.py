@@ -88,18 +88,29 @@ def _episode_steps(caps, sizes, kept):
     return steps
 
 
-def cpu_baseline(w, lay, b_stop, budget_s):
+def cpu_baseline(w, lay, b_stop, budget_s, single_thread=False):
     """The oracle (float64 NumPy, as written) over a bounded sample of the batch:
     chunks of up to 4 images, passing over the batch again until the oracle has
-    run for the time budget."""
+    run for the time budget.  With single_thread the BLAS pool is limited to
+    one thread (the selection loop is single-threaded Python either way)."""
+    import contextlib
+    limit = contextlib.nullcontext()
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        if single_thread:
+            limit = threadpool_limits(1)
+            threads = 1
+    except Exception:
+        threads = 1 if single_thread else (os.cpu_count() or 1)
+    with limit:
+        return _oracle_sample(w, b_stop, budget_s, threads)
+
+
+def _oracle_sample(w, b_stop, budget_s, threads):
     import numpy as np
     import oracle
     from paper_2609_13804_amd import workloads as W
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:
-        threads = os.cpu_count() or 1
     done = 0
     elapsed = 0.0
     chunk = max(1, min(4, w.batch))
@@ -167,8 +178,8 @@ def hbm_traffic(kernel, workload):
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llava15_bf16")
     ap.add_argument("--streams", type=int, default=3,
                     help="consecutive batches go round-robin to this many streams, each with its "
@@ -234,13 +245,19 @@ def main(argv=None):
     if any(run.device_errors()):
         raise RuntimeError(f"device error words {run.device_errors()}")
 
-    def avg_us(a, b):
-        return 1e3 * sum(hip.ms(e[a], e[b]) for e in evs) / K
+    def per_step_us(a, b):
+        return np.array([1e3 * hip.ms(e[a], e[b]) for e in evs])
 
-    stages = {"project": avg_us("step0", "projd"), "select": avg_us("projd", "seld"),
-              "compact": avg_us("seld", "step1"), "step": avg_us("step0", "step1")}
-    kernels = {"project_gemm": avg_us("proj0", "proj1"), "gram_gemm": avg_us("gram0", "gram1"),
-               "select_recurrence": avg_us("rec0", "rec1"), "compact_gather": avg_us("gath0", "gath1")}
+    spans = {"project": ("step0", "projd"), "select": ("projd", "seld"),
+             "compact": ("seld", "step1"), "select_compact": ("projd", "step1"),
+             "step": ("step0", "step1")}
+    stage_t = {k: per_step_us(*v) for k, v in spans.items()}
+    stages = {k: float(v.mean()) for k, v in stage_t.items()}
+    stage_pct = {k: {"p10": float(np.percentile(v, 10)), "p50": float(np.median(v)),
+                     "p90": float(np.percentile(v, 90))} for k, v in stage_t.items()}
+    kern_spans = {"project_gemm": ("proj0", "proj1"), "gram_gemm": ("gram0", "gram1"),
+                  "select_recurrence": ("rec0", "rec1"), "compact_gather": ("gath0", "gath1")}
+    kernels = {k: float(per_step_us(*v).mean()) for k, v in kern_spans.items()}
     for e in evs:
         for ev in e.values():
             hip.destroy(ev)
@@ -253,11 +270,14 @@ def main(argv=None):
     eb = 2 if w.dtype == "bf16" else 4
     L = np.diff(lay.text_off)
 
+    mfma_peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_MATRIX_TFLOPS
+    proj_flop = 2.0 * (s.T_vis + 2) * w.d * 3 * w.h * 1e-12
+    text_flop = 2.0 * s.T_txt * w.d_text * w.h * 1e-12
+    gram_flop = sum(2.0 * (2 * (n + 1) + 3) * (n + 2) * w.h for n in sizes) * 1e-12
     work = {
-        "project_gemm": ("mfma", 2.0 * (s.T_vis + 2) * w.d * 3 * w.h * 1e-12,
-                         PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_MATRIX_TFLOPS, "TFLOP/s"),
-        "gram_gemm": ("mfma", sum(2.0 * 2 * (n + 1) * (n + 2) * w.h for n in sizes) * 1e-12,
-                      PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_MATRIX_TFLOPS, "TFLOP/s"),
+        # the projection launch also computes the text projection's tiles
+        "project_gemm": ("mfma", proj_flop + text_flop, mfma_peak, "TFLOP/s"),
+        "gram_gemm": ("mfma", gram_flop, mfma_peak, "TFLOP/s"),
         "select_recurrence": ("alu", sum(2.0 * (n + 1) * st * (st + 1) / 2
                                          for n, st in zip(sizes, steps_g)) * 1e-12,
                               PEAK_F32_VALU_TFLOPS, "TFLOP/s"),
@@ -274,6 +294,25 @@ def main(argv=None):
 
     elapsed = t1 - t0
     single = {"images_per_s": round(K * s.B / elapsed, 2), "ms_per_step": round(1e3 * elapsed / K, 4)}
+
+    # Roofline fraction of each stage against the unit that bounds its main
+    # kernel: the project stage against the matrix cores (both products), the
+    # select stage against the matrix cores for its Gram products plus the
+    # vector ALU for the recurrence (time-weighted peak), compaction against HBM.
+    def frac(amount, peak, us):
+        return round(amount / (us * 1e-6) / peak, 4)
+    sel_amount = work["select_recurrence"][1]
+    stage_roofline = {
+        "project": {"bound": "mfma", "frac": frac(proj_flop + text_flop, mfma_peak, stages["project"])},
+        "select": {"bound": "mfma+alu",
+                   "frac_gram": frac(gram_flop, mfma_peak, kernels["gram_gemm"]),
+                   "frac_recurrence": frac(sel_amount, PEAK_F32_VALU_TFLOPS,
+                                           kernels["select_recurrence"]),
+                   "recurrence_us_per_step_longest_episode":
+                       round(kernels["select_recurrence"] / max(1, max(steps_g)), 3)},
+        "compact": {"bound": "hbm", "frac": frac(work["compact_gather"][1], PEAK_HBM_GBS,
+                                                 stages["compact"])},
+    }
 
     # Pipelined pass: batch k on stream k mod S, so one batch's projection and
     # Gram products run on the compute units that another batch's recurrence
@@ -328,12 +367,17 @@ def main(argv=None):
                    "longest_episode_steps": int(max(steps_g))},
         "single_stream": single,
         "stages_us": {k: round(v, 2) for k, v in stages.items()},
+        "stages_us_pct": {k: {q: round(x, 2) for q, x in v.items()} for k, v in stage_pct.items()},
+        "stage_roofline": stage_roofline,
         "kernels_us": {k: round(v, 2) for k, v in kernels.items()},
         "selection_steps_per_s": round(sum(steps_g) / (stages["select"] * 1e-6), 1),
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, lay, b_stop, args.cpu_budget)
+        one = cpu_baseline(w, lay, b_stop, args.cpu_budget * 0.5, single_thread=True)
+        out["cpu_baseline"]["single_core"] = {"value": one["value"], "unit": one["unit"],
+                                              "sample": one["sample"]}
     print(json.dumps(out), flush=True)
     return 0
 
