@@ -38,6 +38,9 @@ PEAK_F32_MATRIX_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 # float32 FMA without packed instructions: 256 CU x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz
 PEAK_F32_VALU_TFLOPS = 78.6
+# LDS reads: 256 B/clk per CU measured on gfx950 with the GEMM's ds_read_b128
+# pattern, x 256 CUs x 2.4 GHz
+PEAK_LDS_GBS = 157286.0
 
 
 class HipEvents:
@@ -302,14 +305,29 @@ def main(argv=None):
     def frac(amount, peak, us):
         return round(amount / (us * 1e-6) / peak, 4)
     sel_amount = work["select_recurrence"][1]
+    # The selector against a roofline that assumes a per-step scan of the
+    # unselected keys from LDS plus one HBM read of the keys and the history
+    # rows (the traffic model this build's Gram rewrite replaces): the time
+    # the scan's bytes would take at the LDS and HBM peaks, over the measured
+    # select stage.
+    eb_keys = eb
+    lds_scan = sum(sum((n - t + 2) * w.h * eb_keys for t in range(1, st + 1))
+                   for n, st in zip(sizes, steps_g))
+    hbm_keys = sum(n * w.h * eb_keys + (k + 1) * 2 * w.h * eb_keys
+                   for n, k in zip(sizes, kept_g))
+    t_scan_roof = max(lds_scan / (PEAK_LDS_GBS * 1e9), hbm_keys / (PEAK_HBM_GBS * 1e9))
     stage_roofline = {
-        "project": {"bound": "mfma", "frac": frac(proj_flop + text_flop, mfma_peak, stages["project"])},
+        "project": {"bound": "mfma", "frac": frac(proj_flop + text_flop, mfma_peak, stages["project"]),
+                    "frac_gemm_kernel": frac(proj_flop + text_flop, mfma_peak,
+                                             kernels["project_gemm"])},
         "select": {"bound": "mfma+alu",
                    "frac_gram": frac(gram_flop, mfma_peak, kernels["gram_gemm"]),
                    "frac_recurrence": frac(sel_amount, PEAK_F32_VALU_TFLOPS,
                                            kernels["select_recurrence"]),
                    "recurrence_us_per_step_longest_episode":
-                       round(kernels["select_recurrence"] / max(1, max(steps_g)), 3)},
+                       round(kernels["select_recurrence"] / max(1, max(steps_g)), 3),
+                   "frac_keyscan_roofline": round(t_scan_roof / (stages["select"] * 1e-6), 4),
+                   "keyscan_roofline_us": round(t_scan_roof * 1e6, 2)},
         "compact": {"bound": "hbm", "frac": frac(work["compact_gather"][1], PEAK_HBM_GBS,
                                                  stages["compact"])},
     }

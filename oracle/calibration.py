@@ -12,6 +12,11 @@ is taken at the first step with b > m_t (STOP loses exact ties), hence
 K(b) = #{t : min(m_1..m_t) >= b}, and the batch total sum_g K_g(b) is the
 number of prefix minima >= b.  The bias is placed halfway between two
 adjacent prefix minima so that no STOP decision sits near a tie.
+
+With g tokens per round (Eq. 11) STOP still decides only against the largest
+token logit of a round, so the same m_t applies per round; a round that does
+not stop keeps its whole group, so each prefix minimum is counted once per
+token of that round's group.
 """
 import math
 from typing import List, Sequence, Tuple
@@ -21,21 +26,23 @@ import numpy as np
 from .selection import run_episode
 
 
-def stop_thresholds(KQV, ctx, grp_off, grp_img, grp_cap, h: int) -> List[np.ndarray]:
-    """Per group, the prefix minima of m_t over the steps of a never-stopping run."""
+def stop_thresholds(KQV, ctx, grp_off, grp_img, grp_cap, h: int, g: int = 1) -> List[np.ndarray]:
+    """Per group, the prefix minima of m_t over the rounds of a never-stopping
+    run, each repeated once per token its round keeps."""
     KQV = np.asarray(KQV, np.float64)
     T_vis = KQV.shape[0] - 2
     Kall, Qall, Vall = KQV[:, :h], KQV[:, h:2 * h], KQV[:, 2 * h:3 * h]
     start = (Kall[T_vis], Qall[T_vis], Vall[T_vis])
     k_stop = Kall[T_vis + 1]
     out = []
-    for g in range(len(grp_img)):
-        r0, r1 = int(grp_off[g]), int(grp_off[g + 1])
-        steps = min(int(grp_cap[g]), r1 - r0)
+    for gi in range(len(grp_img)):
+        r0, r1 = int(grp_off[gi]), int(grp_off[gi + 1])
+        rounds = min(int(grp_cap[gi]), -(-(r1 - r0) // g))
         ep = run_episode(Kall[r0:r1], Qall[r0:r1], Vall[r0:r1], start, k_stop,
-                         ctx[int(grp_img[g])], steps, -math.inf, h, keep_vectors=False)
+                         ctx[int(grp_img[gi])], rounds, -math.inf, h, keep_vectors=False, g=g)
         m = np.array([s.token_max - s.stop_raw for s in ep.steps], np.float64)
-        out.append(np.minimum.accumulate(m) if m.size else m)
+        pm = np.minimum.accumulate(m) if m.size else m
+        out.append(np.repeat(pm, [len(x) for x in ep.groups]))
     return out
 
 
