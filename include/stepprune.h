@@ -128,9 +128,9 @@ sp_status stepprune_project(const sp_dims* dims,
                             const hipEvent_t* events, hipStream_t stream);
 
 /*
- * Algorithm 1 steps 2-4 (Eq. 2, Eq. 4).  Every group (a contiguous run of one
- * image's visual rows) is an independent episode: history [START], then per
- * round t = 1..cap the pointer query
+ * Algorithm 1 steps 2-4 (Eq. 2, Eq. 4; Eq. 11 for g > 1).  Every group (a
+ * contiguous run of one image's visual rows) is an independent episode:
+ * history [START], then per round t = 1..cap the pointer query
  *     u_t = c_b + q_e + sum_tau softmax_tau(sigma <q_e, k_tau>) v_tau
  * (e the newest history entry, tau over the history), logits
  * l_t(j) = sigma <u_t, k_j> over the group's unselected tokens and
@@ -138,25 +138,39 @@ sp_status stepprune_project(const sp_dims* dims,
  * taken; STOP ends the episode; a token is masked and appended to the history.
  * At the cap the episode ends without a STOP step.
  *
+ * With g > 1 tokens per round (Section "Grouped Execution for High-Resolution
+ * Inputs", Eq. 11) a round ends the episode only when STOP is strictly above
+ * every unselected token; otherwise it takes the min(g, unselected) tokens of
+ * largest logit (equal logits: lower index first), appends them to the
+ * history in descending-logit order, and the next query q_e is the mean of
+ * their q rows.  The cap counts rounds, so a group keeps at most min(cap g, n).
+ *
  *  KQV, ctx       outputs of stepprune_project (T_vis visual rows + START + STOP)
  *  img_off [B+1]  visual row offsets per image
  *  grp_off [G+1]  visual row offsets per group; groups of an image are
  *                 contiguous and in row order, grp_img [G] their image,
  *                 grp_cap [G] their round cap (>= 0)
  *  max_group      (host) upper bound on any group's size, <= 1022
- *  max_cap        (host) upper bound on any group's effective cap min(cap, n)
+ *  max_cap        (host) upper bound on any group's kept capacity
+ *                 min(cap g, n); a group above it is a device error
  *  kept_off [B+1] offsets of each image's slice of kept_idx; the slice must
- *                 hold sum over its groups of min(cap, n)
+ *                 hold sum over its groups of min(cap g, n)
  *  b_stop         additive STOP bias (may be +-inf)
- *  g              tokens kept per non-STOP round; only g = 1 is supported
+ *  g              tokens kept per non-STOP round, 1 <= g <= 5
+ *                 (SP_EUNSUPPORTED above 5)
  *  flags          SP_TRACE, SP_NO_HISTORY
  *  kept_idx  out  image-local kept indices, ascending per image, at kept_off[b]
  *  kept_cnt  out  [B] kept count per image
  *  grp_cnt   out  [G] kept count per group, or NULL
- *  trace     out  with SP_TRACE: [G, trace_steps, 4] float32 records per step:
- *                 {taken candidate (int32 bits; -1 = STOP), its logit,
- *                  the runner-up candidate logit (-inf if none), STOP logit};
- *                 steps past the end hold taken = -2.  NULL otherwise.
+ *  trace     out  with SP_TRACE, NULL otherwise.  g = 1: [G, trace_steps, 4]
+ *                 float32 records per step: {taken candidate (int32 bits;
+ *                 -1 = STOP), its logit, the runner-up candidate logit (-inf
+ *                 if none), STOP logit}.  g > 1: [G, trace_steps, g + 3] per
+ *                 round: {g slots of taken tokens in appended order (int32
+ *                 bits; slot 0 = -1 for STOP, unused slots -3), the smallest
+ *                 taken logit (the STOP logit for STOP), the largest logit
+ *                 left out (STOP included when not taken; -inf if none), STOP
+ *                 logit}.  Either way records past the end hold -2 in slot 0.
  */
 sp_status stepprune_select(const sp_dims* dims,
                            const void* KQV, const float* ctx, int64_t T_vis,

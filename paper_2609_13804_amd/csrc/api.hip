@@ -127,7 +127,7 @@ sp_status stepprune_select(const sp_dims* dims, const void* KQV, const float* ct
   if (T_vis < 0 || B < 1 || G < 0 || max_group < 0 || max_cap < 0 || trace_steps < 0)
     return SP_EINVAL;
   if (g < 1) return SP_EINVAL;
-  if (g > 1) return SP_EUNSUPPORTED;
+  if (g > kGMax) return SP_EUNSUPPORTED;
   if (max_group > kMaxGroup) return SP_EUNSUPPORTED;
   if (flags & ~(uint32_t)(SP_TRACE | SP_NO_HISTORY)) return SP_EINVAL;
   if (!KQV || !ctx || !img_off || !kept_off || !kept_cnt || !ws) return SP_EINVAL;
@@ -155,6 +155,7 @@ sp_status stepprune_select(const sp_dims* dims, const void* KQV, const float* ct
   a.max_cap = max_cap > 0 ? max_cap : 1;
   a.kept_off = kept_off;
   a.b_stop = b_stop;
+  a.g = g;
   a.flags = flags;
   a.kept_idx = kept_idx;
   a.kept_cnt = kept_cnt;

@@ -49,6 +49,7 @@ struct SelParams {
   float sigma;
   float c1;            // sigma * log2(e)
   float b_stop;
+  int g;               // tokens kept per round (grouped kernels; 1 otherwise)
   uint32_t flags;
   int32_t* grp_kept;   // [G, max_cap] group-local kept indices, ascending
   int32_t* grp_count;  // [G]
@@ -70,8 +71,9 @@ struct SelParams {
 //   key   [2]               decision keys by step parity
 //   red   [16]              per-wave best and runner-up (tracing)
 //   cnt   [16]              end-of-episode counts
+//   ckeys [16][kGMax + 1]   grouped rounds: each wave's best keys, descending
 struct SelLds {
-  int hmain, hsec, alpha, sm, hcol, shist, key, red, cnt, total;
+  int hmain, hsec, alpha, sm, hcol, shist, key, red, cnt, ckeys, total;
   __host__ __device__ SelLds(int W, int lt, int ks, int alpha_ld, int hcap) {
     hmain = 0;
     hsec = hmain + 64 * W * lt * 4;
@@ -82,7 +84,8 @@ struct SelLds {
     key = (shist + hcap * 4 + 15) & ~15;
     red = key + 16;
     cnt = red + 16 * 16;
-    total = cnt + 16 * 4;
+    ckeys = cnt + 16 * 4;
+    total = ckeys + 16 * (kGMax + 1) * 8;
   }
 };
 
@@ -186,8 +189,18 @@ __device__ __forceinline__ int key_index(uint64_t k) {
 // 0 gathers the history scores from the chosen A row and writes the next
 // softmax into LDS; barrier.  The B values are first needed at the end of the
 // next step's logits, after the older history terms.
-template <int RREG, bool SEC, bool TRACE, int MAXT>
+//
+// Grouped kernels (GMAX > 1, Eq. 11) keep g tokens per round: the newest
+// history entries are a group of ng tokens whose mean query row drives the
+// next round (its A row is the mean of the members' A rows, so the history
+// scores and the A term of the logits are means too); each wave then finds
+// its g best candidates, writes their keys to LDS, and after the barrier
+// every wave ranks all of them the same way, stops if STOP's key beats the
+// best, and otherwise takes the g best as the round's group.
+template <int RREG, bool SEC, bool TRACE, int MAXT, int GMAX>
 __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
+  constexpr bool GROUPED = GMAX > 1;
+  static_assert(GMAX >= 1 && GMAX <= kGMax, "group size");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int g = blockIdx.x;
   const int tid = threadIdx.x;
@@ -202,7 +215,9 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     int code = 0;
     if (g0 < 0 || g1 < g0 || g1 > p.T_vis || b < 0 || b >= p.B) code = SP_DEV_BAD_OFFSETS;
     else if (n > p.max_group) code = SP_DEV_GROUP_TOO_LARGE;
-    else if (cap < 0 || (cap < n ? cap : n) > p.max_cap) code = SP_DEV_BAD_CAP;
+    else if (cap < 0 || (int64_t)p.max_cap <
+                          ((int64_t)cap * (GROUPED ? p.g : 1) < n ? (int64_t)cap * (GROUPED ? p.g : 1) : n))
+      code = SP_DEV_BAD_CAP;
     else if (g0 < p.img_off[b] || g1 > p.img_off[b + 1]) code = SP_DEV_BAD_OFFSETS;
     if (code) {
       if (tid == 0) {
@@ -223,6 +238,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   int* hcol = reinterpret_cast<int*>(smem + L.hcol);
   float* shist = reinterpret_cast<float*>(smem + L.shist);
   unsigned long long* key = reinterpret_cast<unsigned long long*>(smem + L.key);
+  unsigned long long* ckeys = reinterpret_cast<unsigned long long*>(smem + L.ckeys);
   float4* red = reinterpret_cast<float4*>(smem + L.red);
   int* cnt = reinterpret_cast<int*>(smem + L.cnt);
 
@@ -287,6 +303,17 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   float a_main = 0.0f, a_sec = 0.0f, a_stop = 0.0f;
   float b_main = 0.0f, b_sec = 0.0f, b_stop = 0.0f;
   int hl = 0;
+  // Grouped rounds: the newest group (ng entries at the end of the history),
+  // its rows, and its B values, stored into the history at the next decision.
+  const int gsz = GROUPED ? p.g : 1;
+  int ng = 1;
+  [[maybe_unused]] int grow[GMAX];
+  [[maybe_unused]] float bg[GMAX], bgs[GMAX], bst[GMAX];
+#pragma unroll
+  for (int i = 0; i < GMAX; ++i) {
+    grow[i] = n;
+    bg[i] = bgs[i] = bst[i] = 0.0f;
+  }
 
   // History softmax of the newest entry e (row r): unnormalised weights
   // e_tau = exp(sigma (A[e, tau] - max)) into alpha, and into sm the reciprocal
@@ -386,14 +413,147 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     }
   };
 
-  load_entry(n, n + 1);   // history entry 0 is START: row n of A and B, column n + 1
+  // Grouped rounds: history softmax for the mean query of the newest group,
+  // x_tau = sigma mean_i A[row_i, col(tau)]; the newest group's own weights
+  // stay in alpha (their B values are added separately), sm[1] is the STOP
+  // term of the entries before it.  Wave 0 only.
+  auto softmax_group = [&]() {
+    const int hpad = (hl + 15) & ~15;
+    const int old = hl - ng;
+    const float cm = c1 / (float)ng;
+    float m, sum = 0.0f, s2 = 0.0f;
+    if (hl <= 256) {
+      // every member slot's scores requested together (slots past the group
+      // hold a valid row and are masked out of the sums)
+      float r0 = 0.0f, r1 = 0.0f, r2 = 0.0f, r3 = 0.0f;
+#pragma unroll
+      for (int i = 0; i < GMAX; ++i) {
+        const float* Ar = A + (int64_t)grow[i] * ld;
+        const float y0 = Ar[hc0], y1 = Ar[hc1], y2 = Ar[hc2], y3 = Ar[hc3];
+        if (i < ng) {
+          r0 += y0; r1 += y1; r2 += y2; r3 += y3;
+        }
+      }
+      const float x0 = lane < hl ? r0 * cm : -INFINITY;
+      const float x1 = lane + 64 < hl ? r1 * cm : -INFINITY;
+      const float x2 = lane + 128 < hl ? r2 * cm : -INFINITY;
+      const float x3 = lane + 192 < hl ? r3 * cm : -INFINITY;
+      m = wave_max_fused(fmaxf(fmaxf(x0, x1), fmaxf(x2, x3)));
+      auto one = [&](int k, float x, float sh) {
+        const int tau = lane + 64 * k;
+        const float e = tau < hl ? __builtin_amdgcn_exp2f(x - m) : 0.0f;
+        sum += e;
+        s2 = fmaf(e, tau < old ? sh : 0.0f, s2);
+        if (tau < hpad) alpha[opaque(tau)] = e;
+      };
+      one(0, x0, sh0);
+      if (64 < hpad) one(1, x1, sh1);
+      if (128 < hpad) one(2, x2, sh2);
+      if (192 < hpad) one(3, x3, sh3);
+    } else {
+      // longer histories: the scores are gathered again in each pass
+      auto score = [&](int tau) {
+        const int c = hcol[tau];
+        float r = 0.0f;
+#pragma unroll
+        for (int i = 0; i < GMAX; ++i)
+          if (i < ng) r += A[(int64_t)grow[i] * ld + c];
+        return r * cm;
+      };
+      m = -INFINITY;
+      for (int tau = lane; tau < hl; tau += 64) m = fmaxf(m, score(tau));
+      m = wave_max_fused(m);
+      for (int tau = lane; tau < hpad; tau += 64) {
+        const float e = tau < hl ? __builtin_amdgcn_exp2f(score(tau) - m) : 0.0f;
+        sum += e;
+        s2 = fmaf(e, tau < old ? shist[tau < old ? tau : 0] : 0.0f, s2);
+        alpha[tau] = e;
+      }
+    }
+    wave_sum2_fused(sum, s2);
+    if (lane == 0) {
+      sm[0] = __builtin_amdgcn_rcpf(sum);
+      sm[1] = s2;
+    }
+  };
+  // Grouped rounds: load a group of cnt members (rows, columns) as the newest
+  // entries: this thread's mean A value over the members and each member's B
+  // values of its columns (left in flight); wave 0 computes the next softmax.
+  auto load_group = [&](const int (&rows)[GMAX], const int (&cols)[GMAX], int cnt) {
+    float am = 0.0f, as2 = 0.0f, ast = 0.0f;
+#pragma unroll
+    for (int i = 0; i < GMAX; ++i) {
+      if (i < cnt) {
+        const float* Ar = A + (int64_t)rows[i] * ld;
+        const float* Br = Bm + (int64_t)rows[i] * ld;
+        am += mcol ? Ar[j] : 0.0f;
+        bg[i] = mcol ? Br[j] : 0.0f;
+        if (SEC) {
+          as2 += scol ? Ar[js] : 0.0f;
+          bgs[i] = scol ? Br[js] : 0.0f;
+        }
+        ast += Ar[n];
+        bst[i] = Br[n];
+        const int pos = hl + i;
+        const int k = pos >> 6;
+        const bool mine = lane == (pos & 63);
+        if (__builtin_amdgcn_readfirstlane(k == 0) && mine) hc0 = cols[i];
+        if (__builtin_amdgcn_readfirstlane(k == 1) && mine) hc1 = cols[i];
+        if (__builtin_amdgcn_readfirstlane(k == 2) && mine) hc2 = cols[i];
+        if (__builtin_amdgcn_readfirstlane(k == 3) && mine) hc3 = cols[i];
+        if (tid == 0) hcol[pos] = cols[i];
+        grow[i] = rows[i];
+      }
+    }
+    a_main = am / (float)cnt;
+    a_sec = as2 / (float)cnt;
+    a_stop = ast / (float)cnt;
+    hl += cnt;
+    ng = cnt;
+    if (wave == 0) softmax_group();
+  };
+  // Grouped rounds: store the newest group's B values into the history.
+  auto store_group = [&]() {
+#pragma unroll
+    for (int i = 0; i < GMAX; ++i) {
+      if (i < ng) {
+        const int pos = hl - ng + i;
+        if (pos < RREG) hput(pos, bg[i]);
+        else if (pos < RREG + lt) hmain[opaque(j) * lt + (pos - RREG)] = bg[i];
+        if (swave && pos < ks && sq == ((pos >> 2) & 3))
+          hsec[(((pos >> 4) * 256 + opaque(tid)) << 2) + (pos & 3)] = bgs[i];
+        if (tid == 0) shist[pos] = bst[i];
+        if (wave == 0) {
+          const int k = pos >> 6;
+          const bool mine = lane == (pos & 63);
+          if (__builtin_amdgcn_readfirstlane(k == 0) && mine) sh0 = bst[i];
+          if (__builtin_amdgcn_readfirstlane(k == 1) && mine) sh1 = bst[i];
+          if (__builtin_amdgcn_readfirstlane(k == 2) && mine) sh2 = bst[i];
+          if (__builtin_amdgcn_readfirstlane(k == 3) && mine) sh3 = bst[i];
+        }
+      }
+    }
+  };
+
+  if constexpr (GROUPED) {
+    // history entry 0 is START: row n of A and B, column n + 1
+    int rows[GMAX], cols[GMAX];
+#pragma unroll
+    for (int i = 0; i < GMAX; ++i) rows[i] = cols[i] = 0;
+    rows[0] = n;
+    cols[0] = n + 1;
+    load_group(rows, cols, 1);
+  } else {
+    load_entry(n, n + 1);   // history entry 0 is START: row n of A and B, column n + 1
+  }
   lds_barrier();
   bool selected = false, sel_sec = false;
   int kept = 0;
 
   for (int t = 1; t <= cap; ++t) {
     const int par = t & 1;
-    const float inv = sm[0], st = sm[1], e_new = sm[2];
+    const float inv = sm[0], st = sm[1];
+    const float e_new = GROUPED ? 0.0f : sm[2];
 
     // ---- logits of the lane-owned columns: older entries from the history
     // tiers (the newest entry's slots still hold zero), then the newest.
@@ -452,13 +612,13 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
         acc = fmaf(av.z, hv.z, acc);
         accb = fmaf(av.w, hv.w, accb);
       }
-      for (tau = RREG + lt; tau < hl - 1; tau += 8) {
+      for (tau = RREG + lt; tau < hl - ng; tau += 8) {
         float hv[8], av[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
           hv[u] = 0.0f;
           av[u] = 0.0f;
-          if (tau + u < hl - 1) {
+          if (tau + u < hl - ng) {
             const int c = hcol[tau + u];
             av[u] = alpha[tau + u];
             if (mcol) hv[u] = Bm[(int64_t)(c == n + 1 ? n : c) * ld + j];
@@ -468,9 +628,25 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
         for (int u = 0; u < 8; ++u) acc = fmaf(av[u], hv[u], acc);
       }
     }
-    acc = fmaf(e_new, b_main, acc + accb);
+    float sp;
+    [[maybe_unused]] float wg[GMAX];     // grouped: the newest group's weights
+    if constexpr (GROUPED) {
+#pragma unroll
+      for (int i = 0; i < GMAX; ++i) wg[i] = i < ng ? alpha[hl - ng + i] : 0.0f;
+      acc += accb;
+      sp = st;
+#pragma unroll
+      for (int i = 0; i < GMAX; ++i) {
+        if (i < ng) {
+          acc = fmaf(wg[i], bg[i], acc);
+          sp = fmaf(wg[i], bst[i], sp);
+        }
+      }
+    } else {
+      acc = fmaf(e_new, b_main, acc + accb);
+      sp = fmaf(e_new, b_stop, st);
+    }
     const float lj = sigma * (ck_main + a_main + acc * inv);
-    const float sp = fmaf(e_new, b_stop, st);
     const float l_stop = sigma * (ck_stop + a_stop + sp * inv) + p.b_stop;
 
     // ---- second columns (waves 0-3): each lane sums its quarter of every
@@ -480,7 +656,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     float ls = -INFINITY;
     if (swave) {
       float acc2 = 0.0f, acc2b = 0.0f;
-      const int last = hl - 1;                 // the newest entry is added below
+      const int last = hl - ng;                // the newest entries are added below
       const int lend = last < ks ? last : ks;
       const int st4 = opaque(tid);                 // 4 scl + sq in waves 0-3
       const float* as = alpha + 4 * (st4 & 3);
@@ -512,57 +688,168 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
       float qs = acc2 + acc2b;
       qs += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(qs), 0xB1, 0xF, 0xF, true));
       qs += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(qs), 0x4E, 0xF, 0xF, true));
-      qs = fmaf(e_new, b_sec, qs);
+      if constexpr (GROUPED) {
+#pragma unroll
+        for (int i = 0; i < GMAX; ++i)
+          if (i < ng) qs = fmaf(wg[i], bgs[i], qs);
+      } else {
+        qs = fmaf(e_new, b_sec, qs);
+      }
       ls = scol && !sel_sec ? sigma * (ck_sec + a_sec + qs * inv) : -INFINITY;
     }
 
-    // ---- this wave's best candidate (lowest index on ties) into the key
-    const bool valid = mcol && !selected;
-    const float v = valid ? lj : -INFINITY;
-    const float vmax = wave_max_fused(swave ? fmaxf(v, ls) : v);
-    int i1 = -1;
-    if (vmax > -INFINITY) {
-      const uint64_t m1 = __ballot(valid && v == vmax);
-      if (m1) i1 = wave * 64 + __ffsll((unsigned long long)m1) - 1;
-      else if (SEC) i1 = 512 + (wave << 4) + ((__ffsll((unsigned long long)__ballot(ls == vmax)) - 1) >> 2);
-      if (lane == 0) atomicMax(&key[par], (unsigned long long)cand_key(vmax, i1));
-    }
-    if (tid == 0 && l_stop > -INFINITY) atomicMax(&key[par], (unsigned long long)cand_key(l_stop, n));
-    if (TRACE) {
-      // runner-up of this wave: the best candidate other than i1
-      const float w1 = valid && j != i1 ? lj : -INFINITY;
-      const float w2 = SEC && js != i1 ? ls : -INFINITY;
-      const float v2 = wave_max_fused(fmaxf(w1, w2));
-      if (lane == 0) red[wave] = make_float4(vmax, __int_as_float(i1), v2, 0.0f);
-    }
-    lds_barrier();
-
-    // ---- the decision (every wave reads the same key)
-    const uint64_t kk = key[par];
-    const int a = kk ? key_index(kk) : n;       // no finite candidate: STOP
-    if (tid == 0) key[par ^ 1] = 0ull;          // next step's key (last read a step ago)
-    if (TRACE && tid == 0 && t <= p.trace_steps) {
-      // runner-up: the largest value among the candidates other than a
-      float r2 = a == n ? -INFINITY : l_stop;
-      for (int w = 0; w < W; ++w) {
-        const float4 r = red[w];
-        r2 = fmaxf(r2, __float_as_int(r.y) == a ? r.z : r.x);
+    if constexpr (GROUPED) {
+      // ---- this wave's best gl candidates, descending (lowest index on ties)
+      const int gl = gsz + (TRACE ? 1 : 0);
+      const bool valid = mcol && !selected;
+      float v1 = valid ? lj : -INFINITY;
+      float ls1 = ls;
+      unsigned long long* ck = ckeys + wave * (kGMax + 1);
+#pragma unroll
+      for (int r = 0; r <= GMAX; ++r) {
+        if (r < gl) {
+          const float vm = wave_max_fused(swave ? fmaxf(v1, ls1) : v1);
+          unsigned long long kr = 0ull;
+          if (vm > -INFINITY) {
+            const uint64_t m1 = __ballot(v1 == vm);
+            int idx;
+            if (m1) idx = wave * 64 + __ffsll((unsigned long long)m1) - 1;
+            else idx = 512 + (wave << 4) + ((__ffsll((unsigned long long)__ballot(ls1 == vm)) - 1) >> 2);
+            kr = cand_key(vm, idx);
+            if (j == idx) v1 = -INFINITY;
+            if (SEC && js == idx) ls1 = -INFINITY;
+          }
+          if (lane == 0) ck[r] = kr;
+        }
       }
-      float* rec = p.trace + ((int64_t)g * p.trace_steps + (t - 1)) * 4;
-      rec[0] = __int_as_float(a == n ? -1 : a);
-      rec[1] = kk ? key_value(kk) : l_stop;
-      rec[2] = r2;
-      rec[3] = l_stop;
+      lds_barrier();
+
+      // ---- the decision: every wave ranks all W * gl keys the same way
+      // (keys are distinct: distinct indices), then reads them by rank
+      unsigned long long kv[3];
+      int rk[3];
+#pragma unroll
+      for (int q = 0; q < 3; ++q) {
+        const int i = lane + 64 * q;
+        kv[q] = i < W * gl ? ckeys[(i / gl) * (kGMax + 1) + i % gl] : 0ull;
+        rk[q] = 0;
+      }
+      for (int w = 0; w < W; ++w)
+        for (int r = 0; r < gl; ++r) {
+          const unsigned long long o = ckeys[w * (kGMax + 1) + r];
+#pragma unroll
+          for (int q = 0; q < 3; ++q) rk[q] += o > kv[q] ? 1 : 0;
+        }
+      // the key of rank r among the valid keys (0 if there is none)
+      auto rank_key = [&](int r) -> unsigned long long {
+        unsigned long long out = 0ull;
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+          const uint64_t mq = __ballot(kv[q] != 0ull && rk[q] == r);
+          if (mq) {
+            const int l = __ffsll((unsigned long long)mq) - 1;
+            const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(kv[q] >> 32), l);
+            const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)kv[q], l);
+            out = ((unsigned long long)hi << 32) | lo;
+          }
+        }
+        return out;
+      };
+      // Valid keys hold ranks 0 .. valid - 1, so the group is ranks < min(g, valid).
+      int gi[GMAX];
+      int cnt = 0;
+      float top_v = -INFINITY, gmin = -INFINITY, ru = -INFINITY;
+      unsigned long long top0 = 0ull;
+#pragma unroll
+      for (int r = 0; r <= GMAX; ++r) {
+        const unsigned long long kr = r < gl ? rank_key(r) : 0ull;
+        if (r == 0) {
+          top0 = kr;
+          top_v = kr ? key_value(kr) : -INFINITY;
+        }
+        if (r < GMAX) gi[r] = kr != 0ull && r < gsz ? key_index(kr) : n;
+        if (r < gsz && kr != 0ull) {
+          ++cnt;
+          gmin = key_value(kr);
+        }
+        if (TRACE && r == gsz && kr != 0ull) ru = key_value(kr);
+      }
+      // STOP ends the episode only as the round's largest logit (it loses ties)
+      const unsigned long long stop_key = l_stop > -INFINITY ? cand_key(l_stop, n) : 0ull;
+      const bool stop = top0 == 0ull || stop_key > top0;
+      if (TRACE && tid == 0 && t <= p.trace_steps) {
+        const int tw = gsz + 3;
+        float* rec = p.trace + ((int64_t)g * p.trace_steps + (t - 1)) * tw;
+#pragma unroll
+        for (int r = 0; r < GMAX; ++r)
+          if (r < gsz) rec[r] = __int_as_float(stop ? (r == 0 ? -1 : -3) : (r < cnt ? gi[r] : -3));
+        rec[gsz] = stop ? l_stop : gmin;
+        rec[gsz + 1] = stop ? top_v : fmaxf(ru, l_stop);
+        rec[gsz + 2] = l_stop;
+      }
+      if (stop) break;
+      kept += cnt;
+#pragma unroll
+      for (int r = 0; r < GMAX; ++r) {
+        if (r < cnt) {
+          if (j == gi[r]) selected = true;
+          if (SEC && js == gi[r]) sel_sec = true;
+        }
+      }
+      if (!no_history) {
+        store_group();
+        load_group(gi, gi, cnt);
+      }
+      lds_barrier();     // the next softmax is in LDS
+    } else {
+      // ---- this wave's best candidate (lowest index on ties) into the key
+      const bool valid = mcol && !selected;
+      const float v = valid ? lj : -INFINITY;
+      const float vmax = wave_max_fused(swave ? fmaxf(v, ls) : v);
+      int i1 = -1;
+      if (vmax > -INFINITY) {
+        const uint64_t m1 = __ballot(valid && v == vmax);
+        if (m1) i1 = wave * 64 + __ffsll((unsigned long long)m1) - 1;
+        else if (SEC) i1 = 512 + (wave << 4) + ((__ffsll((unsigned long long)__ballot(ls == vmax)) - 1) >> 2);
+        if (lane == 0) atomicMax(&key[par], (unsigned long long)cand_key(vmax, i1));
+      }
+      if (tid == 0 && l_stop > -INFINITY) atomicMax(&key[par], (unsigned long long)cand_key(l_stop, n));
+      if (TRACE) {
+        // runner-up of this wave: the best candidate other than i1
+        const float w1 = valid && j != i1 ? lj : -INFINITY;
+        const float w2 = SEC && js != i1 ? ls : -INFINITY;
+        const float v2 = wave_max_fused(fmaxf(w1, w2));
+        if (lane == 0) red[wave] = make_float4(vmax, __int_as_float(i1), v2, 0.0f);
+      }
+      lds_barrier();
+
+      // ---- the decision (every wave reads the same key)
+      const uint64_t kk = key[par];
+      const int a = kk ? key_index(kk) : n;       // no finite candidate: STOP
+      if (tid == 0) key[par ^ 1] = 0ull;          // next step's key (last read a step ago)
+      if (TRACE && tid == 0 && t <= p.trace_steps) {
+        // runner-up: the largest value among the candidates other than a
+        float r2 = a == n ? -INFINITY : l_stop;
+        for (int w = 0; w < W; ++w) {
+          const float4 r = red[w];
+          r2 = fmaxf(r2, __float_as_int(r.y) == a ? r.z : r.x);
+        }
+        float* rec = p.trace + ((int64_t)g * p.trace_steps + (t - 1)) * 4;
+        rec[0] = __int_as_float(a == n ? -1 : a);
+        rec[1] = kk ? key_value(kk) : l_stop;
+        rec[2] = r2;
+        rec[3] = l_stop;
+      }
+      if (a == n) break;
+      ++kept;
+      if (j == a) selected = true;
+      if (SEC && js == a) sel_sec = true;
+      if (!no_history) {
+        store_entry();
+        load_entry(a, a);
+      }
+      lds_barrier();     // the next softmax is in LDS
     }
-    if (a == n) break;
-    ++kept;
-    if (j == a) selected = true;
-    if (SEC && js == a) sel_sec = true;
-    if (!no_history) {
-      store_entry();
-      load_entry(a, a);
-    }
-    lds_barrier();     // the next softmax is in LDS
   }
 
   // ---- native order (Algorithm 1 step 4): ascending positions of the set
@@ -597,13 +884,13 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   }
 }
 
-// Trace records past an episode's end carry taken = -2.
-__global__ void trace_fill_kernel(float* trace, int64_t count) {
+// Trace records (width floats) past an episode's end carry taken = -2.
+__global__ void trace_fill_kernel(float* trace, int64_t count, int width) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < count) {
-    float* rec = trace + i * 4;
+    float* rec = trace + i * width;
     rec[0] = __int_as_float(-2);
-    rec[1] = rec[2] = rec[3] = 0.0f;
+    for (int k = 1; k < width; ++k) rec[k] = 0.0f;
   }
 }
 
@@ -680,7 +967,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   if (trace) {
     const int64_t count = (int64_t)a.G * a.trace_steps;
     hipLaunchKernelGGL(trace_fill_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0,
-                       stream, a.trace, count);
+                       stream, a.trace, count, a.g > 1 ? a.g + 3 : 4);
   }
 
   SelParams p;
@@ -696,6 +983,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.max_group = a.max_group;
   p.max_cap = a.max_cap;
   p.b_stop = a.b_stop;
+  p.g = a.g;
   p.flags = a.flags;
   p.grp_kept = a.grp_kept;
   p.grp_count = a.grp_count;
@@ -720,7 +1008,9 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   }
   const bool wide = W > 8;
   const int need = a.max_cap + 1;                       // longest possible history
-  int rreg = wide ? 32 : need <= 64 ? 64 : need <= 128 ? 128 : 160;
+  const bool grouped = a.g > 1;
+  // grouped kernels hold the newest group's B values too: at most 128 history registers
+  int rreg = wide ? 32 : need <= 64 ? 64 : need <= 128 || grouped ? 128 : 160;
   p.W = W;
   p.hcap = (int)align_up((size_t)need + 1, 4);
   // alpha covers the register blocks' prefetch (up to rreg) and the second
@@ -757,13 +1047,21 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
 
   const void* fn = nullptr;
 #define SP_PICK(RR, SEC, MAXT)                                                           \
-  if (rreg == RR && sec == SEC && (MAXT == 1024) == wide)                                \
-    fn = trace ? (const void*)select_kernel<RR, SEC, true, MAXT>                         \
-               : (const void*)select_kernel<RR, SEC, false, MAXT>;
+  if (!grouped && rreg == RR && sec == SEC && (MAXT == 1024) == wide)                    \
+    fn = trace ? (const void*)select_kernel<RR, SEC, true, MAXT, 1>                      \
+               : (const void*)select_kernel<RR, SEC, false, MAXT, 1>;
   SP_PICK(64, false, 512) SP_PICK(128, false, 512) SP_PICK(160, false, 512)
   SP_PICK(64, true, 512) SP_PICK(128, true, 512) SP_PICK(160, true, 512)
   SP_PICK(32, false, 1024)
 #undef SP_PICK
+#define SP_PICK_G(RR, SEC, MAXT)                                                         \
+  if (grouped && rreg == RR && sec == SEC && (MAXT == 1024) == wide)                     \
+    fn = trace ? (const void*)select_kernel<RR, SEC, true, MAXT, kGMax>                  \
+               : (const void*)select_kernel<RR, SEC, false, MAXT, kGMax>;
+  SP_PICK_G(64, false, 512) SP_PICK_G(128, false, 512)
+  SP_PICK_G(64, true, 512) SP_PICK_G(128, true, 512)
+  SP_PICK_G(32, false, 1024)
+#undef SP_PICK_G
   if (!fn) return hipErrorInvalidValue;
   record_event(a.events, 2, stream);
   if ((e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) != hipSuccess)

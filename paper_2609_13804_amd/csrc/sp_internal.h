@@ -81,6 +81,10 @@ hipError_t launch_text_pool(float* T, int split, const int32_t* text_off, int B,
                             int h, float g_text, float ln_eps, float* ctx, int32_t* err,
                             hipStream_t stream);
 
+// Largest number of tokens kept per round (Eq. 11's group size g; the paper's
+// high-resolution setting uses 5).
+constexpr int kGMax = 5;
+
 struct SelectArgs {
   int dtype;
   const void* KQV;
@@ -97,6 +101,7 @@ struct SelectArgs {
   int max_cap;
   const int32_t* kept_off;
   float b_stop;
+  int g;                 // tokens per round, 1..kGMax
   uint32_t flags;
   int32_t* kept_idx;
   int32_t* kept_cnt;

@@ -40,6 +40,8 @@ class DeviceRun:
         self.b_stop = float(b_stop)
         self.flags = flags | (sp.SP_TRACE if trace_steps > 0 else 0)
         self.trace_steps = trace_steps
+        self.g = w.g
+        self.trace_width = 4 if w.g == 1 else w.g + 3
         dev = torch.device(device)
         tdt = torch_dtype(w.dtype)
         up = lambda a, dt=tdt: torch.from_numpy(np.ascontiguousarray(a)).to(device=dev, dtype=dt)
@@ -55,7 +57,7 @@ class DeviceRun:
         self.caps_host = caps
         kept_per_img = np.zeros(layout.batch + 1, np.int64)
         for g in range(layout.groups):
-            kept_per_img[layout.grp_img[g] + 1] += min(int(caps[g]), int(sizes[g]))
+            kept_per_img[layout.grp_img[g] + 1] += min(int(caps[g]) * w.g, int(sizes[g]))
         kept_off = np.cumsum(kept_per_img).astype(np.int32)
         self.img_off = upi(layout.img_off)
         self.text_off = upi(layout.text_off)
@@ -68,7 +70,7 @@ class DeviceRun:
                            B=layout.batch, G=layout.groups,
                            max_group=int(max_group if max_group is not None else
                                          (sizes.max() if sizes.size else 0)),
-                           max_cap=int(max(1, max((min(int(c), int(n)) for c, n in zip(caps, sizes)),
+                           max_cap=int(max(1, max((min(int(c) * w.g, int(n)) for c, n in zip(caps, sizes)),
                                                   default=1))),
                            kept_total=int(kept_off[-1]))
         s = self.sizes
@@ -96,7 +98,8 @@ class DeviceRun:
         self.kept_idx = torch.full((max(1, s.kept_total),), -1, dtype=torch.int32, device=dev)
         self.kept_cnt = torch.zeros(s.B, dtype=torch.int32, device=dev)
         self.grp_cnt = torch.zeros(max(1, s.G), dtype=torch.int32, device=dev)
-        self.trace = (torch.empty((s.G, self.trace_steps, 4), dtype=torch.float32, device=dev)
+        self.trace = (torch.empty((s.G, self.trace_steps, self.trace_width), dtype=torch.float32,
+                                  device=dev)
                       if self.trace_steps > 0 else None)
         self.seq_info = torch.zeros(s.B + (self.layout_code == sp.SP_LAYOUT_PACKED), dtype=torch.int32,
                                     device=dev)
@@ -125,7 +128,7 @@ class DeviceRun:
         return sp.stepprune_select(self.dims, self.KQV, self.ctx, s.T_vis, self.img_off, s.B,
                                    self.grp_off, self.grp_img, self.grp_cap, s.G, s.max_group,
                                    s.max_cap, self.kept_off,
-                                   self.b_stop if b_stop is None else b_stop, 1,
+                                   self.b_stop if b_stop is None else b_stop, self.g,
                                    self.flags if flags is None else flags, self.kept_idx,
                                    self.kept_cnt, self.grp_cnt, self.trace, self.trace_steps,
                                    self.ws[1], self.ws_bytes[1], stream, events=events)
@@ -155,16 +158,20 @@ class DeviceRun:
         return [idx[off[b]:off[b] + cnt[b]].tolist() for b in range(self.sizes.B)]
 
     def trace_actions(self):
-        """Per group: the taken candidates in order (-1 = STOP)."""
+        """Per group: the taken candidates in order (-1 = STOP); with g > 1 per
+        round the list of taken tokens, [-1] for STOP."""
         tr = self.trace.cpu().numpy()
-        taken = tr[..., 0].view(np.int32)
+        ids = np.ascontiguousarray(tr[..., :self.g]).view(np.int32)
         out = []
         for g in range(self.sizes.G):
             seq = []
             for t in range(self.trace_steps):
-                a = int(taken[g, t])
+                a = int(ids[g, t, 0])
                 if a == -2:
                     break
-                seq.append(a)
+                if self.g == 1:
+                    seq.append(a)
+                else:
+                    seq.append([int(x) for x in ids[g, t] if x != -3])
             out.append(seq)
         return out

@@ -64,6 +64,7 @@ class Workload:
     group_size: int = 0              # "fixed": tokens per group, "balanced": max
     cap: int = 0                     # per-group round cap (0 with cap_frac)
     cap_frac: float = 0.0            # cap = n_group * cap_frac (exact for these sizes)
+    g: int = 1                       # tokens per round (Eq. 11); the cap counts rounds
     layout: str = "padded"           # "padded" | "packed"
     stop_target: Tuple[str, float] = ("mean_k", 64.0)
     description: str = ""
@@ -124,8 +125,37 @@ _add(Workload("mid_bf16", 104, batch=3, d=1024, d_text=1024, h=1024, dtype="bf16
               stop_target=("mean_k", 64.0),
               description="hidden 1024 bf16 with full 576-token groups and long caps"))
 
+# Grouped selection, g = 5 tokens per round (the setting of the high-resolution
+# backbones), on the same shapes: small parity cases, then the three
+# high-resolution batches.
+_add(Workload("tiny_g5_f32", 201, batch=3, d=256, d_text=192, h=64, dtype="f32",
+              text_len=7, tokens=(97, 130, 3), cap=9, g=5, layout="padded",
+              stop_target=("mean_k", 14.0), description="ragged tiny fp32, 5 tokens per round"))
+_add(Workload("small_g5_bf16", 202, batch=5, d=512, d_text=512, h=256, dtype="bf16",
+              text_len=19, ragged=(64, 1400, 4), grouping="balanced", group_size=576,
+              cap_frac=0.05, g=5, layout="packed", stop_target=("ratio", 0.111),
+              description="ragged bf16, balanced groups <= 576, 5 tokens per round, packed"))
+_add(Workload("mid_g5_bf16", 203, batch=2, d=1024, d_text=1024, h=1024, dtype="bf16",
+              text_len=40, tokens=(576, 301), cap=40, g=5, layout="padded",
+              stop_target=("mean_k", 64.0),
+              description="hidden 1024 bf16, full 576-token groups, 5 tokens per round"))
+_add(Workload("llavanext_g5_bf16", 13, batch=8, d=4096, d_text=4096, h=1024, dtype="bf16",
+              text_len=128, tokens=(2880,) * 8, grouping="fixed", group_size=576,
+              cap=13, g=5, layout="padded", stop_target=("mean_k", 32.0),
+              description="8 images x 2880 tokens (5 groups of 576), bf16, 5 tokens per round"))
+_add(Workload("qwen25vl_g5_bf16", 14, batch=32, d=3584, d_text=3584, h=1024, dtype="bf16",
+              text_len=96, ragged=(256, 4096, 4), grouping="balanced", group_size=576,
+              cap_frac=0.05, g=5, layout="packed", stop_target=("ratio", 0.111),
+              description="32 images, N ~ U{256..4096 step 4}, groups <= 576, 5 tokens per round"))
+_add(Workload("internvl3_g5_bf16", 15, batch=64, d=3584, d_text=3584, h=1024, dtype="bf16",
+              text_len=512, tokens=(3328,) * 64, grouping="fixed", group_size=256,
+              cap=7, g=5, layout="packed", stop_target=("ratio", 0.10),
+              description="64 images x 13 groups x 256 tokens, d=3584, 5 tokens per round"))
+
 PAPER_WORKLOADS = ["single_f32", "llava15_bf16", "llavanext_bf16", "qwen25vl_bf16", "internvl3_bf16"]
 SMALL_WORKLOADS = ["tiny_f32", "tiny_bf16", "small_packed_bf16", "mid_bf16"]
+GROUPED_SMALL_WORKLOADS = ["tiny_g5_f32", "small_g5_bf16", "mid_g5_bf16"]
+GROUPED_WORKLOADS = ["llavanext_g5_bf16", "qwen25vl_g5_bf16", "internvl3_g5_bf16"]
 
 
 def image_sizes(w: Workload) -> List[int]:
@@ -172,7 +202,7 @@ class Layout:
     grp_off: np.ndarray     # [G+1] visual row offsets of each group
     grp_img: np.ndarray     # [G] owning image
     grp_cap: np.ndarray     # [G] round cap
-    kept_off: np.ndarray    # [B+1] prefix sum of per-image kept capacity sum_g min(cap, n)
+    kept_off: np.ndarray    # [B+1] prefix sum of per-image kept capacity sum min(cap * g, n)
     rows_per_image: int     # padded layout: rows per image (max N + max L)
     out_rows: int           # rows of the compacted buffer
 
@@ -203,7 +233,7 @@ def make_layout(w: Workload, images: Optional[List[int]] = None) -> Layout:
             grp_img.append(b)
             c = group_cap(w, ng)
             grp_cap.append(c)
-            cap_b += min(c, ng)
+            cap_b += min(c * w.g, ng)
         kept[b + 1] = kept[b] + cap_b
     rows_per_image = max(sizes) + w.text_len
     if w.layout == "padded":

@@ -29,7 +29,7 @@ def calibrate(w):
     KQV = oracle.project(inp["X"], inp["s_start"], inp["s_stop"], inp["W_kqv"], w.dtype)
     ctx = oracle.text_context(inp["E_text"], lay.text_off, inp["W_text"])
     del inp
-    pm = oracle.stop_thresholds(KQV, ctx, lay.grp_off, lay.grp_img, lay.grp_cap, w.h)
+    pm = oracle.stop_thresholds(KQV, ctx, lay.grp_off, lay.grp_img, lay.grp_cap, w.h, g=w.g)
     kind, val = w.stop_target
     n_tok = int(lay.img_off[-1])
     if kind == "mean_k":
@@ -60,4 +60,5 @@ def main(names):
 
 
 if __name__ == "__main__":
-    main(sys.argv[1:] or (W.SMALL_WORKLOADS + W.PAPER_WORKLOADS))
+    main(sys.argv[1:] or (W.SMALL_WORKLOADS + W.PAPER_WORKLOADS + W.GROUPED_SMALL_WORKLOADS
+                          + W.GROUPED_WORKLOADS))

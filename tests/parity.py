@@ -17,6 +17,12 @@ Tolerances (the bar every GPU parity test applies):
   * kept indices and counts: equal to the GPU's own action sets, and equal to
     the free-running oracle for every episode without an exempt step;
   * compaction: bit-exact.
+
+With g tokens per round (Eq. 11) the same protocol applies per round: the
+GPU's group must be the oracle's as a set, except in rounds where the STOP
+decision or the membership of the g-th token is a near-tie (relative gap
+below 1e-4 between the top token and STOP, or between the g-th and (g+1)-th
+token), which are counted like exempt steps.
 """
 from dataclasses import dataclass, field
 from typing import List, Optional, Sequence
@@ -132,10 +138,95 @@ def check_selection(KQV: np.ndarray, ctx: np.ndarray, grp_off, grp_img, caps, b_
     return rep
 
 
+def _flat(seq):
+    """Taken tokens of an action sequence (ints, or per-round lists)."""
+    out = []
+    for a in seq:
+        out.extend(a if isinstance(a, (list, tuple)) else [a])
+    return [a for a in out if a != -1]
+
+
 def kept_from_actions(actions, grp_off, grp_img, img_off, B):
     kept = [[] for _ in range(B)]
     for g, seq in enumerate(actions):
         b = int(grp_img[g])
         base = int(grp_off[g]) - int(img_off[b])
-        kept[b].extend(base + a for a in sorted(a for a in seq if a != -1))
+        kept[b].extend(base + a for a in sorted(_flat(seq)))
     return kept
+
+
+def check_grouped_selection(KQV: np.ndarray, ctx: np.ndarray, grp_off, grp_img, caps, b_stop: float,
+                            h: int, gsize: int, rounds: Sequence[Sequence[Sequence[int]]],
+                            trace: Optional[np.ndarray], dtype: str, no_history: bool = False,
+                            groups: Optional[Sequence[int]] = None) -> SelectReport:
+    """The staged, teacher-forced check with g = gsize tokens per round.
+
+    ``rounds[g]`` is the GPU's round sequence of group g: per round the taken
+    tokens, or [-1] for STOP; ``trace[g, r]`` its round record {taken tokens
+    (-1 STOP, -3 unused slot), smallest taken logit (the STOP logit when STOP
+    is taken), largest logit left out, STOP logit}."""
+    tol = logit_tol(dtype)
+    rep = SelectReport()
+    T_vis = KQV.shape[0] - 2
+    Kall, Qall, Vall = KQV[:, :h], KQV[:, h:2 * h], KQV[:, 2 * h:3 * h]
+    start = (Kall[T_vis], Qall[T_vis], Vall[T_vis])
+    k_stop = Kall[T_vis + 1]
+    gs = range(len(grp_img)) if groups is None else groups
+    for g in gs:
+        r0, r1 = int(grp_off[g]), int(grp_off[g + 1])
+        n = r1 - r0
+        cap = int(caps[g])
+        seq = [list(r) for r in rounds[g]]
+        c = ctx[int(grp_img[g])]
+        args = (Kall[r0:r1], Qall[r0:r1], Vall[r0:r1], start, k_stop, c, cap, b_stop, h)
+        forced = [STOP if r == [-1] else r for r in seq]
+        ep = oracle.run_episode(*args, no_history=no_history, forced=forced, g=gsize)
+        rep.episodes += 1
+        where = f"group {g} (n={n}, cap={cap}, g={gsize})"
+        assert len(ep.steps) == len(seq), f"{where}: oracle replay took {len(ep.steps)} rounds, GPU {len(seq)}"
+        assert (seq and seq[-1] == [-1]) or len(seq) == cap, f"{where}: GPU episode ended early"
+        taken = _flat(seq)
+        assert len(set(taken)) == len(taken), f"{where}: repeat"
+        exempt_here = 0
+        for t, (r, st) in enumerate(zip(seq, ep.steps)):
+            rep.steps += 1
+            scale = _scale(st)
+            gpu_stop = r == [-1]
+            or_stop = st.argmax == STOP
+            if gpu_stop != or_stop or (not gpu_stop and sorted(r) != sorted(st.best_group)):
+                near = st.margin_stop < MARGIN_EXEMPT if gpu_stop != or_stop else st.margin_member < MARGIN_EXEMPT
+                assert near, (f"{where} round {t + 1}: GPU took {r}, oracle {st.best_group or 'STOP'} "
+                              f"(stop margin {st.margin_stop:.3e}, member margin {st.margin_member:.3e})")
+                exempt_here += 1
+                rep.exempt_steps += 1
+                rep.divergences.append(f"{where} round {t + 1}: {r} vs {st.best_group or 'STOP'}")
+            if not gpu_stop:
+                assert len(r) == min(gsize, n - sum(len(x) for x in seq[:t])), f"{where} round {t + 1}: size"
+                # appended in descending-logit order
+                lv = [float(st.logits[x]) for x in r]
+                assert all(lv[i] >= lv[i + 1] - tol * scale for i in range(len(lv) - 1)), (
+                    f"{where} round {t + 1}: group order {r} has logits {lv}")
+            if trace is not None:
+                rec = trace[g, t]
+                ids = [int(x) for x in np.asarray(rec[:gsize], np.float32).view(np.int32)]
+                if gpu_stop:
+                    assert ids[0] == -1 and all(x == -3 for x in ids[1:]), f"{where} round {t + 1}: trace"
+                else:
+                    assert ids[:len(r)] == r and all(x == -3 for x in ids[len(r):]), (
+                        f"{where} round {t + 1}: trace {ids} vs {r}")
+                want_min = st.stop_logit if gpu_stop else st.group_min
+                want_ru = st.runner_up
+                for got, want, what in ((float(rec[gsize]), want_min, "taken"),
+                                        (float(rec[gsize + 1]), want_ru, "runner-up"),
+                                        (float(rec[gsize + 2]), st.stop_logit, "STOP")):
+                    assert _close(got, want, tol * scale), (
+                        f"{where} round {t + 1}: {what} logit {got!r} vs oracle {want!r} (scale {scale:.3g})")
+                    if np.isfinite(want):
+                        rep.max_logit_err = max(rep.max_logit_err, abs(got - want) / scale)
+        if exempt_here == 0:
+            free = oracle.run_episode(*args, no_history=no_history, keep_steps=False, g=gsize)
+            rep.free_running_checked += 1
+            assert [sorted(x) for x in free.groups] == [sorted(x) for x in seq if x != [-1]], (
+                f"{where}: free-running oracle differs without near-ties")
+            rep.free_running_equal += 1
+    return rep

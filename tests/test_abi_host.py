@@ -86,7 +86,8 @@ def _select(sp, dm=None, **kw):
 
 def test_select_validation(sp):
     assert _select(sp, g=0) == sp.SP_EINVAL
-    assert _select(sp, g=5) == sp.SP_EUNSUPPORTED
+    assert _select(sp, g=6) == sp.SP_EUNSUPPORTED                       # g <= 5
+    assert _select(sp, g=5) == sp.SP_EWORKSPACE                         # accepted up to the workspace
     assert _select(sp, max_group=1023) == sp.SP_EUNSUPPORTED
     assert _select(sp, max_group=-1) == sp.SP_EINVAL
     assert _select(sp, flags=8) == sp.SP_EINVAL
