@@ -83,11 +83,13 @@ def _ensure_built():
         build.build()
 
 
-def _episode_steps(caps, sizes, kept):
+def _episode_steps(caps, sizes, kept, g=1):
+    """Rounds per episode: ceil(kept / g) token rounds, plus the STOP round
+    unless the episode ended at its cap."""
     steps = []
     for c, n, k in zip(caps, sizes, kept):
-        c, n, k = int(c), int(n), int(k)
-        steps.append(k if k == c else k + 1)      # at the cap no STOP step is taken
+        r = -(-int(k) // g)
+        steps.append(r if r == int(c) else r + 1)
     return steps
 
 
@@ -128,7 +130,7 @@ def _oracle_sample(w, b_stop, budget_s, threads):
         KQV = oracle.project(inp["X"], inp["s_start"], inp["s_stop"], inp["W_kqv"], w.dtype)
         ctx = oracle.text_context(inp["E_text"], sl.text_off, inp["W_text"])
         res = oracle.select(KQV, ctx, sl.img_off, sl.grp_off, sl.grp_img, sl.grp_cap, b_stop, w.h,
-                            keep_steps=False)
+                            keep_steps=False, g=w.g)
         if w.d_text == w.d:
             oracle.compact(inp["X"], sl.img_off, inp["E_text"], sl.text_off, res.kept, w.layout,
                            sl.rows_per_image, np.zeros((sl.out_rows, w.d)))
@@ -185,8 +187,13 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llava15_bf16")
     ap.add_argument("--streams", type=int, default=3,
-                    help="consecutive batches go round-robin to this many streams, each with its "
-                         "own outputs and workspaces (1: one stream, one batch after another)")
+                    help="streams of the pipelined pass: select streams (staggered, at most 3) "
+                         "or round-robin streams (rr); 1: no pipelined pass")
+    ap.add_argument("--slots", type=int, default=4,
+                    help="buffer slots of the staggered pipelined pass (batches in flight)")
+    ap.add_argument("--schedule", choices=["staggered", "rr"], default="staggered",
+                    help="pipelined pass: projections on one stream ahead of per-slot select "
+                         "streams (staggered), or whole batches round-robin (rr)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle work for the CPU baseline sample")
@@ -269,7 +276,7 @@ def main(argv=None):
     sizes = np.diff(lay.grp_off)
     kept_g = run.grp_cnt.cpu().numpy()[:s.G]
     kept_b = run.kept_cnt.cpu().numpy()
-    steps_g = _episode_steps(run.caps_host, sizes, kept_g)
+    steps_g = _episode_steps(run.caps_host, sizes, kept_g, w.g)
     eb = 2 if w.dtype == "bf16" else 4
     L = np.diff(lay.text_off)
 
@@ -281,7 +288,8 @@ def main(argv=None):
         # the projection launch also computes the text projection's tiles
         "project_gemm": ("mfma", proj_flop + text_flop, mfma_peak, "TFLOP/s"),
         "gram_gemm": ("mfma", gram_flop, mfma_peak, "TFLOP/s"),
-        "select_recurrence": ("alu", sum(2.0 * (n + 1) * st * (st + 1) / 2
+        # round t reads n + 1 columns against a history of 1 + g (t - 1) entries
+        "select_recurrence": ("alu", sum(2.0 * (n + 1) * (st + w.g * st * (st - 1) / 2)
                                          for n, st in zip(sizes, steps_g)) * 1e-12,
                               PEAK_F32_VALU_TFLOPS, "TFLOP/s"),
         "compact_gather": ("hbm", float(((kept_b + L) * w.d * eb * 2).sum() + kept_b.sum() * 4) * 1e-9,
@@ -311,7 +319,7 @@ def main(argv=None):
     # the scan's bytes would take at the LDS and HBM peaks, over the measured
     # select stage.
     eb_keys = eb
-    lds_scan = sum(sum((n - t + 2) * w.h * eb_keys for t in range(1, st + 1))
+    lds_scan = sum(sum((max(n - w.g * (t - 1), 0) + 2) * w.h * eb_keys for t in range(1, st + 1))
                    for n, st in zip(sizes, steps_g))
     hbm_keys = sum(n * w.h * eb_keys + (k + 1) * 2 * w.h * eb_keys
                    for n, k in zip(sizes, kept_g))
@@ -332,21 +340,28 @@ def main(argv=None):
                                                  stages["compact"])},
     }
 
-    # Pipelined pass: batch k on stream k mod S, so one batch's projection and
-    # Gram products run on the compute units that another batch's recurrence
-    # (one workgroup per episode) leaves free.  Each stream owns its outputs
-    # and workspaces; the inputs are shared read-only.
+    # Pipelined pass: projections on one stream in batch order, batch k's
+    # select + compact on the stream of slot k mod S (runner.Pipeline), so one
+    # batch's projection and Gram products run on the compute units that
+    # earlier batches' recurrences (one workgroup per episode) leave free.
+    # --schedule rr instead issues whole batches round-robin on S streams.
     S = max(1, args.streams)
     if S > 1:
-        runs = [run] + [run.sibling() for _ in range(S - 1)]
-        streams = [torch.cuda.Stream() for _ in range(S)]     # default priority
-        def issue(k):
-            r, st = runs[k % S], streams[k % S].cuda_stream
-            r.project(st)
-            r.select(st)
-            if r.out is not None:
-                r.compact(st)
-        for k in range(max(args.warmup, S)):
+        from paper_2609_13804_amd.runner import Pipeline
+        if args.schedule == "staggered":
+            pipe = Pipeline(run, max(S, args.slots), min(S, Pipeline.MAX_STREAMS))
+            runs = pipe.runs
+            issue = lambda k: pipe.issue()
+        else:
+            runs = [run] + [run.sibling() for _ in range(S - 1)]
+            streams = [torch.cuda.Stream() for _ in range(S)]     # default priority
+            def issue(k):
+                r, st = runs[k % S], streams[k % S].cuda_stream
+                r.project(st)
+                r.select(st)
+                if r.out is not None:
+                    r.compact(st)
+        for k in range(max(args.warmup, len(runs))):
             issue(k)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
@@ -378,8 +393,10 @@ def main(argv=None):
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "images": s.B, "groups": s.G, "streams": S,
+                   "schedule": args.schedule if S > 1 else "single",
+                   "slots": max(S, args.slots) if S > 1 and args.schedule == "staggered" else S,
                    "tokens": int(s.T_vis), "d": w.d, "h": w.h, "text_tokens": int(s.T_txt),
-                   "layout": w.layout, "b_stop": b_stop,
+                   "layout": w.layout, "b_stop": b_stop, "tokens_per_round": w.g,
                    "kept_mean_per_image": round(float(kept_b.mean()), 3),
                    "selection_steps": int(sum(steps_g)),
                    "longest_episode_steps": int(max(steps_g))},

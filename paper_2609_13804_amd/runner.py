@@ -175,3 +175,54 @@ class DeviceRun:
                     seq.append([int(x) for x in ids[g, t] if x != -3])
             out.append(seq)
         return out
+
+
+class Pipeline:
+    """A stream of batches through the three stages with the projection of
+    later batches overlapping the selection of earlier ones.
+
+    The recurrence of one batch occupies one compute unit per episode for
+    most of a batch's time while the projection and Gram products need the
+    whole chip, so batches are staggered: every projection runs on one
+    stream, in batch order, and batch k's select + compact run on select
+    stream k mod ``streams``.  Batch k uses buffer slot k mod ``slots``, a
+    DeviceRun with its own outputs and workspaces (inputs shared read-only):
+    a slot's projection waits for the slot's previous select + compact, and
+    its select waits for its projection.  More slots than select streams let
+    the projection run ahead of the recurrences.  All streams use the
+    default priority.
+
+    The projections go to the caller's current stream, so the pipeline uses
+    streams + 1 streams in all: at most three select streams keep every
+    stream on a hardware queue of its own under HIP's default of four per
+    process."""
+
+    MAX_STREAMS = 3
+
+    def __init__(self, run: DeviceRun, slots: int = 4, streams: int = 3):
+        if not 1 <= streams <= self.MAX_STREAMS:
+            raise ValueError(f"streams must be 1..{self.MAX_STREAMS}")
+        if slots < streams:
+            raise ValueError("need at least one slot per select stream")
+        self.runs = [run] + [run.sibling() for _ in range(slots - 1)]
+        self.proj_stream = torch.cuda.current_stream()
+        self.sel_streams = [torch.cuda.Stream() for _ in range(streams)]
+        self.projected = [torch.cuda.Event() for _ in self.runs]
+        self.done = [torch.cuda.Event() for _ in self.runs]
+        self.k = 0
+
+    def issue(self):
+        """Queue the next batch (nothing waits on the host)."""
+        s = self.k % len(self.runs)
+        r, ps = self.runs[s], self.proj_stream
+        ss = self.sel_streams[self.k % len(self.sel_streams)]
+        if self.k >= len(self.runs):
+            ps.wait_event(self.done[s])
+        r.project(ps.cuda_stream)
+        self.projected[s].record(ps)
+        ss.wait_event(self.projected[s])
+        r.select(ss.cuda_stream)
+        if r.out is not None:
+            r.compact(ss.cuda_stream)
+        self.done[s].record(ss)
+        self.k += 1

@@ -1,4 +1,5 @@
-"""The five paper-shaped batches at full size, launched exactly as bench.py
+"""The five paper-shaped batches, and the three high-resolution ones with g = 5
+tokens per round (Eq. 11), at full size, launched exactly as bench.py
 launches them (one stream, untraced selection kernel), checked against the
 oracle on outputs it can compute one by one:
 
@@ -32,16 +33,21 @@ SAMPLE_GROUPS = 16
 SAMPLE_IMAGES = 3
 
 
-def _sample_groups(rng, sizes, caps, steps, k):
+def _rounds(cap, n, g):
+    """Rounds of an episode that never stops: the cap or ceil(n / g)."""
+    return min(int(cap), -(-int(n) // g))
+
+
+def _sample_groups(rng, sizes, caps, steps, k, g):
     """k groups: the longest episode, a capped one if any, the rest at random."""
     G = len(sizes)
     chosen = [int(np.argmax(steps))]
-    capped = [g for g in range(G) if steps[g] == min(int(caps[g]), int(sizes[g])) and caps[g] > 0]
+    capped = [i for i in range(G) if steps[i] == _rounds(caps[i], sizes[i], g) and caps[i] > 0]
     if capped:
         chosen.append(int(capped[len(capped) // 2]))
-    rest = [g for g in range(G) if g not in chosen]
+    rest = [i for i in range(G) if i not in chosen]
     extra = rng.choice(rest, size=min(len(rest), max(0, k - len(chosen))), replace=False)
-    return sorted(set(chosen) | set(int(g) for g in extra))
+    return sorted(set(chosen) | set(int(i) for i in extra))
 
 
 def _sub_episodes(KQV_dev, grp_off, groups, T_vis):
@@ -55,7 +61,7 @@ def _sub_episodes(KQV_dev, grp_off, groups, T_vis):
     return sub, off
 
 
-@pytest.mark.parametrize("name", W.PAPER_WORKLOADS)
+@pytest.mark.parametrize("name", W.PAPER_WORKLOADS + W.GROUPED_WORKLOADS)
 def test_full_size_parity(gpu_lib, name):
     from paper_2609_13804_amd.runner import DeviceRun
     w = W.WORKLOADS[name]
@@ -63,7 +69,7 @@ def test_full_size_parity(gpu_lib, name):
     inp = W.make_inputs(w)
     b_stop = W.stop_bias(w)
     sizes = np.diff(lay.grp_off)
-    steps_max = int(max(min(int(c), int(n)) for c, n in zip(lay.grp_cap, sizes))) + 1
+    steps_max = int(max(_rounds(c, n, w.g) for c, n in zip(lay.grp_cap, sizes))) + 1
     print(f"{name}: {lay.batch} images, {lay.groups} groups, {int(lay.img_off[-1])} tokens",
           flush=True)
     run = DeviceRun(w, inp, lay, b_stop, trace_steps=steps_max)
@@ -106,17 +112,23 @@ def test_full_size_parity(gpu_lib, name):
     assert run.kept_lists() == kept
     assert kept == parity.kept_from_actions(actions, lay.grp_off, lay.grp_img, lay.img_off,
                                             lay.batch)
-    assert grp_cnt.tolist() == [sum(1 for a in s if a != -1) for s in actions]
+    assert grp_cnt.tolist() == [len(parity._flat(s)) for s in actions]
+    stop = -1 if w.g == 1 else [-1]
     for g, s in enumerate(actions):
-        cap = min(int(lay.grp_cap[g]), int(sizes[g]))
-        assert (s and s[-1] == -1 and len(s) <= cap + 1) or len(s) == int(lay.grp_cap[g]), g
+        r = _rounds(lay.grp_cap[g], sizes[g], w.g)
+        assert (s and s[-1] == stop and len(s) <= r + 1) or len(s) == int(lay.grp_cap[g]), g
     steps = np.array([len(s) for s in actions])
 
-    groups = _sample_groups(rng, sizes, lay.grp_cap, steps, SAMPLE_GROUPS)
+    groups = _sample_groups(rng, sizes, lay.grp_cap, steps, SAMPLE_GROUPS, w.g)
     sub, sub_off = _sub_episodes(run.KQV, lay.grp_off, groups, T_vis)
     trace = run.trace.cpu().numpy()[groups]
-    rep = parity.check_selection(sub, ctx, sub_off, lay.grp_img[groups], lay.grp_cap[groups],
-                                 b_stop, w.h, [actions[g] for g in groups], trace, w.dtype)
+    if w.g == 1:
+        rep = parity.check_selection(sub, ctx, sub_off, lay.grp_img[groups], lay.grp_cap[groups],
+                                     b_stop, w.h, [actions[g] for g in groups], trace, w.dtype)
+    else:
+        rep = parity.check_grouped_selection(sub, ctx, sub_off, lay.grp_img[groups],
+                                             lay.grp_cap[groups], b_stop, w.h, w.g,
+                                             [actions[g] for g in groups], trace, w.dtype)
     print(f"{name}: checked {rep.episodes} of {lay.groups} episodes ({rep.steps} steps, longest "
           f"{int(steps.max())}), {rep.exempt_steps} exempt, max logit err "
           f"{rep.max_logit_err:.2e}, free-running equal {rep.free_running_equal}/"
