@@ -71,9 +71,11 @@ struct SelParams {
 //   key   [2]               decision keys by step parity
 //   red   [16]              per-wave best and runner-up (tracing)
 //   cnt   [16]              end-of-episode counts
-//   ckeys [16][kGMax + 1]   grouped rounds: each wave's best keys, descending
+//   ckeys [16][kGMax + 1]   grouped rounds: each wave's best keys, descending (slots
+//                           a launch never writes stay zero)
+//   ranked [16][kGMax + 1]  grouped rounds: each wave's copy of the merged ranks
 struct SelLds {
-  int hmain, hsec, alpha, sm, hcol, shist, key, red, cnt, ckeys, total;
+  int hmain, hsec, alpha, sm, hcol, shist, key, red, cnt, ckeys, ranked, total;
   __host__ __device__ SelLds(int W, int lt, int ks, int alpha_ld, int hcap) {
     hmain = 0;
     hsec = hmain + 64 * W * lt * 4;
@@ -85,7 +87,8 @@ struct SelLds {
     red = key + 16;
     cnt = red + 16 * 16;
     ckeys = cnt + 16 * 4;
-    total = ckeys + 16 * (kGMax + 1) * 8;
+    ranked = ckeys + 16 * (kGMax + 1) * 8;
+    total = ranked + 16 * (kGMax + 1) * 8;
   }
 };
 
@@ -201,6 +204,7 @@ template <int RREG, bool SEC, bool TRACE, int MAXT, int GMAX>
 __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   constexpr bool GROUPED = GMAX > 1;
   static_assert(GMAX >= 1 && GMAX <= kGMax, "group size");
+  static_assert(!(SEC && MAXT == 1024), "second columns only in 8-wave groups");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int g = blockIdx.x;
   const int tid = threadIdx.x;
@@ -239,6 +243,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   float* shist = reinterpret_cast<float*>(smem + L.shist);
   unsigned long long* key = reinterpret_cast<unsigned long long*>(smem + L.key);
   unsigned long long* ckeys = reinterpret_cast<unsigned long long*>(smem + L.ckeys);
+  unsigned long long* ranked = reinterpret_cast<unsigned long long*>(smem + L.ranked);
   float4* red = reinterpret_cast<float4*>(smem + L.red);
   int* cnt = reinterpret_cast<int*>(smem + L.cnt);
 
@@ -269,6 +274,8 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   if (wave == 0)
     for (int i = lane; i < p.alpha_ld; i += 64) alpha[i] = 0.0f;
   if (tid < 2) key[tid] = 0ull;
+  if (GROUPED)
+    for (int i = tid; i < 16 * (kGMax + 1); i += 64 * W) ckeys[i] = 0ull;
 
   // Lane-owned history values in 32-wide vector registers.  Reads use
   // constant slots after unrolling; a write picks the vector with a uniform
@@ -283,8 +290,8 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
          : i < 128 ? h3[i & 31] : h4[i & 31];
   };
   auto hput = [&](int pos, float x) {
-    const int e = pos & 31;
-    const int k = pos >> 5;
+    const int e = __builtin_amdgcn_readfirstlane(pos & 31);   // uniform: one indexed move
+    const int k = __builtin_amdgcn_readfirstlane(pos >> 5);
     if (__builtin_amdgcn_readfirstlane(k == 0)) h0[e] = x;
     if (NV > 1 && __builtin_amdgcn_readfirstlane(k == 1)) h1[e] = x;
     if (NV > 2 && __builtin_amdgcn_readfirstlane(k == 2)) h2[e] = x;
@@ -425,14 +432,27 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     if (hl <= 256) {
       // every member slot's scores requested together (slots past the group
       // hold a valid row and are masked out of the sums)
-      float r0 = 0.0f, r1 = 0.0f, r2 = 0.0f, r3 = 0.0f;
+      float y[GMAX][4];
 #pragma unroll
       for (int i = 0; i < GMAX; ++i) {
         const float* Ar = A + (int64_t)grow[i] * ld;
-        const float y0 = Ar[hc0], y1 = Ar[hc1], y2 = Ar[hc2], y3 = Ar[hc3];
-        if (i < ng) {
-          r0 += y0; r1 += y1; r2 += y2; r3 += y3;
-        }
+        y[i][0] = Ar[hc0];
+        y[i][1] = Ar[hc1];
+        y[i][2] = Ar[hc2];
+        y[i][3] = Ar[hc3];
+      }
+      // all requested before any is used (one round trip)
+#pragma unroll
+      for (int i = 0; i < GMAX; ++i)
+        asm volatile("" : "+v"(y[i][0]), "+v"(y[i][1]), "+v"(y[i][2]), "+v"(y[i][3]));
+      float r0 = 0.0f, r1 = 0.0f, r2 = 0.0f, r3 = 0.0f;
+#pragma unroll
+      for (int i = 0; i < GMAX; ++i) {
+        const bool in = i < ng;
+        r0 += in ? y[i][0] : 0.0f;
+        r1 += in ? y[i][1] : 0.0f;
+        r2 += in ? y[i][2] : 0.0f;
+        r3 += in ? y[i][3] : 0.0f;
       }
       const float x0 = lane < hl ? r0 * cm : -INFINITY;
       const float x1 = lane + 64 < hl ? r1 * cm : -INFINITY;
@@ -454,10 +474,12 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
       // longer histories: the scores are gathered again in each pass
       auto score = [&](int tau) {
         const int c = hcol[tau];
+        float y[GMAX];
+#pragma unroll
+        for (int i = 0; i < GMAX; ++i) y[i] = A[(int64_t)grow[i] * ld + c];
         float r = 0.0f;
 #pragma unroll
-        for (int i = 0; i < GMAX; ++i)
-          if (i < ng) r += A[(int64_t)grow[i] * ld + c];
+        for (int i = 0; i < GMAX; ++i) r += i < ng ? y[i] : 0.0f;
         return r * cm;
       };
       m = -INFINITY;
@@ -479,21 +501,50 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   // Grouped rounds: load a group of cnt members (rows, columns) as the newest
   // entries: this thread's mean A value over the members and each member's B
   // values of its columns (left in flight); wave 0 computes the next softmax.
+  // Every member slot's loads are issued together (slots past cnt hold a
+  // valid row, columns without a candidate read column 0, and both are masked
+  // out), so they share one memory round trip; 16-wave groups load one
+  // member at a time.
   auto load_group = [&](const int (&rows)[GMAX], const int (&cols)[GMAX], int cnt) {
     float am = 0.0f, as2 = 0.0f, ast = 0.0f;
+    [[maybe_unused]] float av[GMAX], asv[GMAX], atv[GMAX];
+    if constexpr (MAXT == 1024) {
+      // 16-wave groups (128 registers a lane): one member at a time, which
+      // keeps fewer values live across the round
+#pragma unroll
+      for (int i = 0; i < GMAX; ++i) {
+        if (i < cnt) {
+          const float* Ar = A + (int64_t)rows[i] * ld;
+          const float* Br = Bm + (int64_t)rows[i] * ld;
+          am += mcol ? Ar[j] : 0.0f;
+          bg[i] = mcol ? Br[j] : 0.0f;
+          ast += Ar[n];
+          bst[i] = Br[n];
+          grow[i] = rows[i];
+        }
+      }
+    } else {
+      const int jc = mcol ? j : 0;
+      const int jsc = scol ? js : 0;
+#pragma unroll
+      for (int i = 0; i < GMAX; ++i) {
+        const float* Ar = A + (int64_t)rows[i] * ld;
+        const float* Br = Bm + (int64_t)rows[i] * ld;
+        av[i] = Ar[jc];
+        bg[i] = Br[jc];
+        asv[i] = 0.0f;
+        if (SEC) {
+          asv[i] = Ar[jsc];
+          bgs[i] = Br[jsc];
+        }
+        atv[i] = Ar[n];
+        bst[i] = Br[n];
+        grow[i] = rows[i];
+      }
+    }
 #pragma unroll
     for (int i = 0; i < GMAX; ++i) {
       if (i < cnt) {
-        const float* Ar = A + (int64_t)rows[i] * ld;
-        const float* Br = Bm + (int64_t)rows[i] * ld;
-        am += mcol ? Ar[j] : 0.0f;
-        bg[i] = mcol ? Br[j] : 0.0f;
-        if (SEC) {
-          as2 += scol ? Ar[js] : 0.0f;
-          bgs[i] = scol ? Br[js] : 0.0f;
-        }
-        ast += Ar[n];
-        bst[i] = Br[n];
         const int pos = hl + i;
         const int k = pos >> 6;
         const bool mine = lane == (pos & 63);
@@ -502,15 +553,25 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
         if (__builtin_amdgcn_readfirstlane(k == 2) && mine) hc2 = cols[i];
         if (__builtin_amdgcn_readfirstlane(k == 3) && mine) hc3 = cols[i];
         if (tid == 0) hcol[pos] = cols[i];
-        grow[i] = rows[i];
       }
     }
-    a_main = am / (float)cnt;
-    a_sec = as2 / (float)cnt;
-    a_stop = ast / (float)cnt;
     hl += cnt;
     ng = cnt;
     if (wave == 0) softmax_group();
+    // the members' A values are summed only now, so wave 0's softmax gathers
+    // went out while they were still in flight
+    if constexpr (MAXT != 1024) {
+#pragma unroll
+      for (int i = 0; i < GMAX; ++i) {
+        const bool in = i < cnt;
+        am += in ? av[i] : 0.0f;
+        as2 += in ? asv[i] : 0.0f;
+        ast += in ? atv[i] : 0.0f;
+      }
+    }
+    a_main = mcol ? am / (float)cnt : 0.0f;
+    a_sec = scol ? as2 / (float)cnt : 0.0f;
+    a_stop = ast / (float)cnt;
   };
   // Grouped rounds: store the newest group's B values into the history.
   auto store_group = [&]() {
@@ -724,37 +785,44 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
       }
       lds_barrier();
 
-      // ---- the decision: every wave ranks all W * gl keys the same way
-      // (keys are distinct: distinct indices), then reads them by rank
-      unsigned long long kv[3];
-      int rk[3];
+      // ---- the decision: every wave ranks all keys the same way (valid keys
+      // are distinct, having distinct indices; empty slots hold 0 and rank
+      // below them), files the first GMAX + 1 by rank into its own list and
+      // reads them back.  The slot count is fixed by the launch shape, so the
+      // reads of the counting pass are independent and overlap.
+      constexpr int NS = (MAXT / 64) * (kGMax + 1);
+      constexpr int NQ = (NS + 63) / 64;
+      static_assert(NS % 8 == 0, "key slots are read eight at a time");
+      unsigned long long kv[NQ];
+      int rk[NQ];
+      int nvalid = 0;
 #pragma unroll
-      for (int q = 0; q < 3; ++q) {
+      for (int q = 0; q < NQ; ++q) {
         const int i = lane + 64 * q;
-        kv[q] = i < W * gl ? ckeys[(i / gl) * (kGMax + 1) + i % gl] : 0ull;
+        kv[q] = i < NS ? ckeys[i] : 0ull;
         rk[q] = 0;
+        nvalid += __popcll(__ballot(kv[q] != 0ull));
       }
-      for (int w = 0; w < W; ++w)
-        for (int r = 0; r < gl; ++r) {
-          const unsigned long long o = ckeys[w * (kGMax + 1) + r];
+      const ulonglong2* ck2 = reinterpret_cast<const ulonglong2*>(ckeys);
+#pragma unroll(MAXT == 1024 ? 1 : NS / 8)
+      for (int s0 = 0; s0 < NS / 2; s0 += 4) {
+        ulonglong2 o[4];
 #pragma unroll
-          for (int q = 0; q < 3; ++q) rk[q] += o > kv[q] ? 1 : 0;
-        }
+        for (int u = 0; u < 4; ++u) o[u] = ck2[s0 + u];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int q = 0; q < NQ; ++q) rk[q] += (o[u].x > kv[q] ? 1 : 0) + (o[u].y > kv[q] ? 1 : 0);
+      }
+      unsigned long long* rl = ranked + wave * (kGMax + 1);
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+        if (kv[q] != 0ull && rk[q] <= GMAX) rl[rk[q]] = kv[q];
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
       // the key of rank r among the valid keys (0 if there is none)
-      auto rank_key = [&](int r) -> unsigned long long {
-        unsigned long long out = 0ull;
-#pragma unroll
-        for (int q = 0; q < 3; ++q) {
-          const uint64_t mq = __ballot(kv[q] != 0ull && rk[q] == r);
-          if (mq) {
-            const int l = __ffsll((unsigned long long)mq) - 1;
-            const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(kv[q] >> 32), l);
-            const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)kv[q], l);
-            out = ((unsigned long long)hi << 32) | lo;
-          }
-        }
-        return out;
-      };
+      auto rank_key = [&](int r) -> unsigned long long { return r < nvalid ? rl[r] : 0ull; };
       // Valid keys hold ranks 0 .. valid - 1, so the group is ranks < min(g, valid).
       int gi[GMAX];
       int cnt = 0;
@@ -1009,8 +1077,9 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   const bool wide = W > 8;
   const int need = a.max_cap + 1;                       // longest possible history
   const bool grouped = a.g > 1;
-  // grouped kernels hold the newest group's B values too: at most 128 history registers
-  int rreg = wide ? 32 : need <= 64 ? 64 : need <= 128 || grouped ? 128 : 160;
+  // grouped kernels hold the newest group's values too, and their histories
+  // grow g entries a round: 64 history registers, then the LDS tier
+  int rreg = wide ? 32 : need <= 64 || grouped ? 64 : need <= 128 ? 128 : 160;
   p.W = W;
   p.hcap = (int)align_up((size_t)need + 1, 4);
   // alpha covers the register blocks' prefetch (up to rreg) and the second
@@ -1058,9 +1127,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   if (grouped && rreg == RR && sec == SEC && (MAXT == 1024) == wide)                     \
     fn = trace ? (const void*)select_kernel<RR, SEC, true, MAXT, kGMax>                  \
                : (const void*)select_kernel<RR, SEC, false, MAXT, kGMax>;
-  SP_PICK_G(64, false, 512) SP_PICK_G(128, false, 512)
-  SP_PICK_G(64, true, 512) SP_PICK_G(128, true, 512)
-  SP_PICK_G(32, false, 1024)
+  SP_PICK_G(64, false, 512) SP_PICK_G(64, true, 512) SP_PICK_G(32, false, 1024)
 #undef SP_PICK_G
   if (!fn) return hipErrorInvalidValue;
   record_event(a.events, 2, stream);
