@@ -160,7 +160,8 @@ sp_status stepprune_project(const sp_dims* dims,
  *                 (SP_EUNSUPPORTED above 5)
  *  flags          SP_TRACE, SP_NO_HISTORY
  *  kept_idx  out  image-local kept indices, ascending per image, at kept_off[b]
- *  kept_cnt  out  [B] kept count per image
+ *  kept_cnt  out  [B] kept count per image (0 for an image whose slice of
+ *                 kept_idx overflows, with SP_DEV_OUTPUT_OVERFLOW)
  *  grp_cnt   out  [G] kept count per group, or NULL
  *  trace     out  with SP_TRACE, NULL otherwise.  g = 1: [G, trace_steps, 4]
  *                 float32 records per step: {taken candidate (int32 bits;

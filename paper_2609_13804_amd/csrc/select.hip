@@ -962,42 +962,94 @@ __global__ void trace_fill_kernel(float* trace, int64_t count, int width) {
   }
 }
 
-// Per image: concatenate its groups' kept lists in group order, offset to
-// image-local indices.
-__global__ __launch_bounds__(256) void finalize_kernel(const int32_t* __restrict__ img_off, int B,
-                                                       const int32_t* __restrict__ grp_off,
-                                                       const int32_t* __restrict__ grp_img, int G,
-                                                       const int32_t* __restrict__ grp_kept,
-                                                       const int32_t* __restrict__ grp_count,
-                                                       int max_cap,
-                                                       const int32_t* __restrict__ kept_off,
-                                                       int32_t* __restrict__ kept_idx,
-                                                       int32_t* __restrict__ kept_cnt,
-                                                       int32_t* err) {
-  const int b = blockIdx.x;
+// Per group (one wave each): copy its kept list into its image's slice of
+// kept_idx, after the kept lists of the image's earlier groups, offset to
+// image-local indices.  The groups of an image are contiguous and images come
+// in order, so a group finds its place by summing the counts of the run of
+// same-image groups just before it (64 at a time, one load per lane).  The
+// image's last group writes the image's count; each group zeroes the counts
+// of the images between the previous group's image and its own (the last
+// group also those after its own), which have no group.  On an overflow of
+// the image's slice the image's count is 0 (and the error word says why).
+__global__ __launch_bounds__(64) void finalize_kernel(const int32_t* __restrict__ img_off, int B,
+                                                      const int32_t* __restrict__ grp_off,
+                                                      const int32_t* __restrict__ grp_img, int G,
+                                                      const int32_t* __restrict__ grp_kept,
+                                                      const int32_t* __restrict__ grp_count,
+                                                      int max_cap,
+                                                      const int32_t* __restrict__ kept_off,
+                                                      int32_t* __restrict__ kept_idx,
+                                                      int32_t* __restrict__ kept_cnt,
+                                                      int32_t* err) {
+  const int lane = threadIdx.x;
+  if (G == 0) {
+    for (int b = lane; b < B; b += 64) kept_cnt[b] = 0;
+    return;
+  }
+  const int g = blockIdx.x;
+  const int b = grp_img[g];
+  const int prev = g > 0 ? grp_img[g - 1] : -1;
+  const int next = g + 1 < G ? grp_img[g + 1] : B;
+  if (b < 0 || b >= B || prev > b || next < b) {
+    if (lane == 0) set_device_error(err, SP_DEV_BAD_OFFSETS);
+    return;
+  }
+  // images strictly between the previous group's and this one have no group,
+  // nor have those after the last group's
+  for (int i = prev + 1 + lane; i < b; i += 64) kept_cnt[i] = 0;
+  if (g == G - 1)
+    for (int i = b + 1 + lane; i < B; i += 64) kept_cnt[i] = 0;
+
+  // counts of the run of this image's groups before g
+  int before = 0;
+  for (int top = g - 1; top >= 0; top -= 64) {
+    const int q = top - lane;
+    const bool same = q >= 0 && grp_img[q] == b;
+    const int c = same ? grp_count[q] : 0;
+    const uint64_t other = __ballot(!same);
+    const int run = other ? __ffsll((unsigned long long)other) - 1 : 64;
+    int v = lane < run ? c : 0;
+    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+    before += v;
+    if (run < 64) break;
+  }
+  const int cnt = grp_count[g];
   const int64_t base = kept_off[b];
   const int64_t room = (int64_t)kept_off[b + 1] - base;
   if (base < 0 || room < 0) {
-    if (threadIdx.x == 0) {
-      set_device_error(err, SP_DEV_BAD_OFFSETS);
-      kept_cnt[b] = 0;
+    if (lane == 0) set_device_error(err, SP_DEV_BAD_OFFSETS);
+    return;
+  }
+  // every group of the image tests the image's total, so a slice that
+  // overflows anywhere receives nothing
+  int total = 0;
+  {
+    // the image's groups after g, counted the same way
+    int after = 0;
+    for (int bot = g + 1; bot < G; bot += 64) {
+      const int q = bot + lane;
+      const bool same = q < G && grp_img[q] == b;
+      const int c = same ? grp_count[q] : 0;
+      const uint64_t other = __ballot(!same);
+      const int run = other ? __ffsll((unsigned long long)other) - 1 : 64;
+      int v = lane < run ? c : 0;
+      for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+      after += v;
+      if (run < 64) break;
+    }
+    total = before + cnt + after;
+  }
+  if (total > room) {
+    if (lane == 0) {
+      set_device_error(err, SP_DEV_OUTPUT_OVERFLOW);
+      if (next > b) kept_cnt[b] = 0;
     }
     return;
   }
-  int64_t filled = 0;
-  for (int g = 0; g < G; ++g) {
-    if (grp_img[g] != b) continue;
-    const int cnt = grp_count[g];
-    const int off = grp_off[g] - img_off[b];
-    if (filled + cnt > room) {
-      if (threadIdx.x == 0) set_device_error(err, SP_DEV_OUTPUT_OVERFLOW);
-      break;
-    }
-    for (int i = threadIdx.x; i < cnt; i += blockDim.x)
-      kept_idx[base + filled + i] = off + grp_kept[(int64_t)g * max_cap + i];
-    filled += cnt;
-  }
-  if (threadIdx.x == 0) kept_cnt[b] = (int32_t)filled;
+  const int off = grp_off[g] - img_off[b];
+  for (int i = lane; i < cnt; i += 64)
+    kept_idx[base + before + i] = off + grp_kept[(int64_t)g * max_cap + i];
+  if (lane == 0 && next > b) kept_cnt[b] = total;
 }
 
 }  // namespace
@@ -1005,7 +1057,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(const int32_t* __restrict
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   if (a.G == 0) {
     if (a.B > 0)
-      hipLaunchKernelGGL(finalize_kernel, dim3(a.B), dim3(256), 0, stream, a.img_off, a.B,
+      hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(64), 0, stream, a.img_off, a.B,
                          a.grp_off, a.grp_img, a.G, a.grp_kept, a.grp_count, a.max_cap, a.kept_off,
                          a.kept_idx, a.kept_cnt, a.err);
     return hipGetLastError();
@@ -1137,7 +1189,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   if ((e = hipLaunchKernel(fn, dim3(a.G), dim3(64 * W), kargs, lds, stream)) != hipSuccess) return e;
   record_event(a.events, 3, stream);
 
-  hipLaunchKernelGGL(finalize_kernel, dim3(a.B), dim3(256), 0, stream, a.img_off, a.B, a.grp_off,
+  hipLaunchKernelGGL(finalize_kernel, dim3(a.G), dim3(64), 0, stream, a.img_off, a.B, a.grp_off,
                      a.grp_img, a.G, a.grp_kept, a.grp_count, a.max_cap, a.kept_off, a.kept_idx,
                      a.kept_cnt, a.err);
   return hipGetLastError();

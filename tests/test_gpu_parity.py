@@ -208,6 +208,44 @@ def test_zero_caps_and_episode_independence(gpu_lib):
     assert run3.kept_lists() == [full[i] for i in sub]
 
 
+def test_images_without_groups(gpu_lib):
+    """Images of 0 tokens have no group (fixed partitions): their kept counts
+    are 0 even over a dirty output, the other images' kept lists match the
+    oracle, and a batch with no group at all gives all-zero counts."""
+    from paper_2609_13804_amd.runner import DeviceRun
+    w = W.Workload("empty_images", 109, batch=6, d=256, d_text=256, h=128, dtype="bf16",
+                   text_len=5, tokens=(0, 200, 0, 0, 150, 0), grouping="fixed", group_size=96,
+                   cap=20, layout="padded", description="images without tokens")
+    lay, inp = W.make_layout(w), W.make_inputs(w)
+    assert lay.groups == 5 and list(lay.grp_img) == [1, 1, 1, 4, 4]
+    run = DeviceRun(w, inp, lay, 0.5, trace_steps=21)
+    run.project()
+    run.kept_cnt.fill_(77)
+    run.select()
+    torch.cuda.synchronize()
+    _check_errors(run)
+    cnt = run.kept_cnt.cpu().numpy().tolist()
+    assert [cnt[b] for b in (0, 2, 3, 5)] == [0, 0, 0, 0]
+    KQV, ctx = _staged(run)
+    actions = run.trace_actions()
+    parity.check_selection(KQV, ctx, lay.grp_off, lay.grp_img, run.caps_host, run.b_stop, w.h,
+                           actions, run.trace.cpu().numpy(), w.dtype)
+    assert run.kept_lists() == parity.kept_from_actions(actions, lay.grp_off, lay.grp_img,
+                                                        lay.img_off, lay.batch)
+    w0 = W.Workload("no_groups", 110, batch=2, d=256, d_text=256, h=128, dtype="bf16",
+                    text_len=5, tokens=(0, 0), grouping="fixed", group_size=96, cap=20,
+                    layout="padded", description="no visual token at all")
+    lay0, inp0 = W.make_layout(w0), W.make_inputs(w0)
+    assert lay0.groups == 0
+    run0 = DeviceRun(w0, inp0, lay0, 0.5)
+    run0.project()
+    run0.kept_cnt.fill_(77)
+    run0.select()
+    torch.cuda.synchronize()
+    _check_errors(run0)
+    assert run0.kept_cnt.cpu().numpy().tolist() == [0, 0]
+
+
 def test_device_error_on_oversized_group(gpu_lib):
     """A group larger than the stated max_group is reported through the device
     error word and no kernel reads past its buffers."""
