@@ -13,6 +13,7 @@ Modules
   rounding     round-to-nearest-even to bfloat16 / float32 storage
   projection   Algorithm 1 step 1: projected keys/queries/values, text context
   selection    Algorithm 1 steps 2-4: the pointer recurrence with STOP (Eq. 4)
+  trajectory   the trajectory sums of the training surrogate (Eqs. 5-7)
   compaction   Algorithm 1 step 5: gather of kept tokens ahead of the prompt
   calibration  the STOP bias that gives a target mean retained count
 
@@ -23,6 +24,7 @@ from .rounding import round_bf16, round_f32, round_to
 from .projection import project, text_context, layer_norm
 from .selection import (StepRecord, EpisodeResult, SelectResult, run_episode,
                         select, STOP)
+from .trajectory import TrajectoryResult, step_distribution, aggregate, run_trajectory
 from .compaction import compact
 from .calibration import stop_thresholds, choose_stop_bias
 
@@ -30,4 +32,5 @@ __all__ = [
     "round_bf16", "round_f32", "round_to", "project", "text_context", "layer_norm",
     "StepRecord", "EpisodeResult", "SelectResult", "run_episode", "select", "STOP",
     "compact", "stop_thresholds", "choose_stop_bias",
+    "TrajectoryResult", "step_distribution", "aggregate", "run_trajectory",
 ]

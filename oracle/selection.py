@@ -139,7 +139,8 @@ def _rel_gap(a: float, b: float, fin: np.ndarray) -> float:
 
 def run_episode(K, Q, V, start, k_stop, c, cap: int, b_stop: float, h: int,
                 no_history: bool = False, forced: Optional[Sequence] = None,
-                keep_steps: bool = True, keep_vectors: bool = True, g: int = 1) -> EpisodeResult:
+                keep_steps: bool = True, keep_vectors: bool = True, g: int = 1,
+                ignore_stop: bool = False) -> EpisodeResult:
     """One episode of the pointer recurrence (Eq. 4 with the STOP rule of Eq. 2;
     g tokens per round as in Eq. 11).
 
@@ -149,7 +150,10 @@ def run_episode(K, Q, V, start, k_stop, c, cap: int, b_stop: float, h: int,
     the selection history).  ``forced`` replays a given action sequence instead
     of taking the argmax: per round a token index (g = 1) or a sequence of
     token indices, STOP as -1.  ``keep_vectors`` stores the logits and the
-    query of every step in its record.
+    query of every step in its record.  ``ignore_stop`` runs the full rollout
+    over which the trajectory sums of Eqs. 5-7 run to T_max: the action is the
+    best token even where STOP is the largest logit (STOP is still scored, and
+    taken only once no token is left).
     """
     if g < 1:
         raise ValueError("g must be at least 1")
@@ -195,7 +199,7 @@ def run_episode(K, Q, V, start, k_stop, c, cap: int, b_stop: float, h: int,
             token_max = -np.inf
         else:
             token_max = float(logits[order[0]])
-            best = STOP if stop_logit > token_max else int(order[0])
+            best = STOP if stop_logit > token_max and not ignore_stop else int(order[0])
         best_group = [] if best == STOP else [int(x) for x in order[:g]]
         cand = np.append(logits, stop_logit)
         t1, t2, margin = _relative_margin(cand)
