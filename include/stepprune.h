@@ -73,8 +73,11 @@ typedef enum { SP_F32 = 0, SP_BF16 = 1 } sp_dtype;
 
 enum {
   SP_TRACE = 1u,       /* stepprune_select writes the per-step trace */
-  SP_NO_HISTORY = 2u   /* pointer query frozen at its first value (diagnostic:
+  SP_NO_HISTORY = 2u,  /* pointer query frozen at its first value (diagnostic:
                           the selector collapses to top-K of the first scores, Eq. 1) */
+  SP_FULL_ROLLOUT = 4u /* the rollout that the trajectory sums of Eqs. 5-7 run over:
+                          STOP is scored but not taken while a token is left, so
+                          every episode runs to its cap (or out of tokens) */
 };
 
 enum { SP_LAYOUT_PADDED = 0, SP_LAYOUT_PACKED = 1 };
@@ -158,7 +161,7 @@ sp_status stepprune_project(const sp_dims* dims,
  *  b_stop         additive STOP bias (may be +-inf)
  *  g              tokens kept per non-STOP round, 1 <= g <= 5
  *                 (SP_EUNSUPPORTED above 5)
- *  flags          SP_TRACE, SP_NO_HISTORY
+ *  flags          SP_TRACE, SP_NO_HISTORY, SP_FULL_ROLLOUT
  *  kept_idx  out  image-local kept indices, ascending per image, at kept_off[b]
  *  kept_cnt  out  [B] kept count per image (0 for an image whose slice of
  *                 kept_idx overflows, with SP_DEV_OUTPUT_OVERFLOW)
@@ -185,6 +188,54 @@ sp_status stepprune_select(const sp_dims* dims,
                            float* trace, int32_t trace_steps,
                            void* ws, size_t ws_bytes,
                            const hipEvent_t* events, hipStream_t stream);
+
+/*
+ * Trajectory sums of the training surrogate (Section "Trajectory-Aware
+ * Differentiable Optimization"), computed along the pointer trajectory that
+ * stepprune_select_trajectory executes (g = 1):
+ *     p_t   = softmax(l_t / tau) over the step's candidates (unselected
+ *             tokens and STOP; Eq. 4)
+ *     A_1 = 1, A_{t+1} = A_t (1 - p_t(STOP))                       (Eq. 5)
+ *     s_i   = sum_t A_t p_t(i) beta^t                               (Eq. 6)
+ *     K_bar = sum_t A_t (1 - p_t(STOP))                             (Eq. 7)
+ * over the executed steps: up to and including the STOP step, or, with
+ * SP_FULL_ROLLOUT, every step up to the cap (T_max).  Caller-owned device
+ * buffers:
+ *  s          out [T_vis] float32, s_i of every token of every group (rows
+ *             outside all groups are not written)
+ *  kbar       out [G] float32, K_bar per group
+ *  pstop      out [G, pstop_steps] float32, p_t(STOP) per step (NaN past
+ *             the episode's end), or NULL
+ */
+typedef struct {
+  float tau;            /* pointer temperature, > 0 */
+  float beta;           /* discount, 0 < beta <= 1 */
+  float* s;
+  float* kbar;
+  float* pstop;
+  int32_t pstop_steps;  /* >= 0; 0 with pstop = NULL */
+} sp_trajectory;
+
+/*
+ * stepprune_select, and along the same trajectory the sums described with
+ * sp_trajectory (Eqs. 5-7).  Arguments as for stepprune_select plus `traj`
+ * (host pointer, required).  g must be 1 (SP_EUNSUPPORTED otherwise);
+ * tau <= 0, beta outside (0, 1] or a NULL s / kbar give SP_EINVAL.  Runs the
+ * traced selection kernel, so it is slower than stepprune_select.
+ */
+sp_status stepprune_select_trajectory(const sp_dims* dims,
+                                      const void* KQV, const float* ctx, int64_t T_vis,
+                                      const int32_t* img_off, int32_t B,
+                                      const int32_t* grp_off, const int32_t* grp_img,
+                                      const int32_t* grp_cap, int32_t G,
+                                      int32_t max_group, int32_t max_cap,
+                                      const int32_t* kept_off,
+                                      float b_stop, int32_t g, uint32_t flags,
+                                      int32_t* kept_idx, int32_t* kept_cnt, int32_t* grp_cnt,
+                                      float* trace, int32_t trace_steps,
+                                      const sp_trajectory* traj,
+                                      void* ws, size_t ws_bytes,
+                                      const hipEvent_t* events, hipStream_t stream);
 
 /*
  * Algorithm 1 step 5.  Gathers each image's kept visual rows (ascending) and

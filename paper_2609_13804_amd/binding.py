@@ -15,12 +15,12 @@ LIB_PATH = os.path.join(HERE, "libstepprune.so")
 
 SP_OK, SP_EINVAL, SP_EUNSUPPORTED, SP_EWORKSPACE, SP_EHIP, SP_EDEVICE = range(6)
 SP_F32, SP_BF16 = 0, 1
-SP_TRACE, SP_NO_HISTORY = 1, 2
+SP_TRACE, SP_NO_HISTORY, SP_FULL_ROLLOUT = 1, 2, 4
 SP_LAYOUT_PADDED, SP_LAYOUT_PACKED = 0, 1
 SP_DEV_OK, SP_DEV_BAD_OFFSETS, SP_DEV_GROUP_TOO_LARGE, SP_DEV_BAD_CAP, SP_DEV_OUTPUT_OVERFLOW = range(5)
 STAGE_PROJECT, STAGE_SELECT, STAGE_COMPACT = 0, 1, 2
 
-EXPORTS = ["stepprune_project", "stepprune_select", "stepprune_compact",
+EXPORTS = ["stepprune_project", "stepprune_select", "stepprune_select_trajectory", "stepprune_compact",
            "stepprune_workspace_bytes", "stepprune_read_device_error", "stepprune_status_string"]
 
 
@@ -33,6 +33,12 @@ class StepPruneError(RuntimeError):
 class sp_dims(ctypes.Structure):
     _fields_ = [("d", ctypes.c_int32), ("d_text", ctypes.c_int32),
                 ("h", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class sp_trajectory(ctypes.Structure):
+    _fields_ = [("tau", ctypes.c_float), ("beta", ctypes.c_float), ("s", ctypes.c_void_p),
+                ("kbar", ctypes.c_void_p), ("pstop", ctypes.c_void_p),
+                ("pstop_steps", ctypes.c_int32)]
 
 
 if not os.path.exists(LIB_PATH):
@@ -52,6 +58,10 @@ _lib.stepprune_project.argtypes = [_DIMS, _P, _I64, _P, _P, _P, _P, _P, _I32, _I
 _lib.stepprune_select.restype = _I32
 _lib.stepprune_select.argtypes = [_DIMS, _P, _P, _I64, _P, _I32, _P, _P, _P, _I32, _I32, _I32, _P,
                                   _F32, _I32, ctypes.c_uint32, _P, _P, _P, _P, _I32, _P, _SZ, _P, _P]
+_lib.stepprune_select_trajectory.restype = _I32
+_lib.stepprune_select_trajectory.argtypes = [_DIMS, _P, _P, _I64, _P, _I32, _P, _P, _P, _I32, _I32,
+                                             _I32, _P, _F32, _I32, ctypes.c_uint32, _P, _P, _P, _P,
+                                             _I32, ctypes.POINTER(sp_trajectory), _P, _SZ, _P, _P]
 _lib.stepprune_compact.restype = _I32
 _lib.stepprune_compact.argtypes = [_DIMS, _P, _P, _P, _P, _P, _P, _P, _I32, _I32, _I32, _I64, _P, _P,
                                    _P, _SZ, _P, _P]
@@ -130,6 +140,23 @@ def stepprune_select(dm, KQV, ctx, T_vis, img_off, B, grp_off, grp_img, grp_cap,
                                _ptr(grp_cnt), _ptr(trace), trace_steps, _ptr(ws), ws_bytes,
                                _events(events), _stream(stream))
     return _check("stepprune_select", st, raise_on_error)
+
+
+def trajectory(tau, beta, s, kbar, pstop=None, pstop_steps=0) -> sp_trajectory:
+    return sp_trajectory(tau, beta, _ptr(s), _ptr(kbar), _ptr(pstop), pstop_steps)
+
+
+def stepprune_select_trajectory(dm, KQV, ctx, T_vis, img_off, B, grp_off, grp_img, grp_cap, G,
+                                max_group, max_cap, kept_off, b_stop, g, flags, kept_idx, kept_cnt,
+                                grp_cnt, trace, trace_steps, traj, ws, ws_bytes, stream=None,
+                                raise_on_error=True, events=None):
+    st = _lib.stepprune_select_trajectory(
+        ctypes.byref(dm), _ptr(KQV), _ptr(ctx), T_vis, _ptr(img_off), B, _ptr(grp_off),
+        _ptr(grp_img), _ptr(grp_cap), G, max_group, max_cap, _ptr(kept_off), b_stop, g, flags,
+        _ptr(kept_idx), _ptr(kept_cnt), _ptr(grp_cnt), _ptr(trace), trace_steps,
+        ctypes.byref(traj) if traj is not None else None, _ptr(ws), ws_bytes, _events(events),
+        _stream(stream))
+    return _check("stepprune_select_trajectory", st, raise_on_error)
 
 
 def stepprune_compact(dm, X, img_off, E_text, text_off, kept_idx, kept_off, kept_cnt, B, layout,

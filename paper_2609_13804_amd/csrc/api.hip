@@ -114,14 +114,20 @@ sp_status stepprune_project(const sp_dims* dims, const void* X, int64_t T_vis, c
   return hip_status(e);
 }
 
-sp_status stepprune_select(const sp_dims* dims, const void* KQV, const float* ctx, int64_t T_vis,
-                           const int32_t* img_off, int32_t B, const int32_t* grp_off,
-                           const int32_t* grp_img, const int32_t* grp_cap, int32_t G,
-                           int32_t max_group, int32_t max_cap, const int32_t* kept_off,
-                           float b_stop, int32_t g, uint32_t flags, int32_t* kept_idx,
-                           int32_t* kept_cnt, int32_t* grp_cnt, float* trace, int32_t trace_steps,
-                           void* ws, size_t ws_bytes, const hipEvent_t* events,
-                           hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Shared body of stepprune_select and stepprune_select_trajectory (traj may be
+// null for the former).
+sp_status select_impl(const sp_dims* dims, const void* KQV, const float* ctx, int64_t T_vis,
+                      const int32_t* img_off, int32_t B, const int32_t* grp_off,
+                      const int32_t* grp_img, const int32_t* grp_cap, int32_t G,
+                      int32_t max_group, int32_t max_cap, const int32_t* kept_off, float b_stop,
+                      int32_t g, uint32_t flags, int32_t* kept_idx, int32_t* kept_cnt,
+                      int32_t* grp_cnt, float* trace, int32_t trace_steps,
+                      const sp_trajectory* traj, void* ws, size_t ws_bytes,
+                      const hipEvent_t* events, hipStream_t stream) {
   sp_status st = check_dims(dims);
   if (st != SP_OK) return st;
   if (T_vis < 0 || B < 1 || G < 0 || max_group < 0 || max_cap < 0 || trace_steps < 0)
@@ -129,11 +135,17 @@ sp_status stepprune_select(const sp_dims* dims, const void* KQV, const float* ct
   if (g < 1) return SP_EINVAL;
   if (g > kGMax) return SP_EUNSUPPORTED;
   if (max_group > kMaxGroup) return SP_EUNSUPPORTED;
-  if (flags & ~(uint32_t)(SP_TRACE | SP_NO_HISTORY)) return SP_EINVAL;
+  if (flags & ~(uint32_t)(SP_TRACE | SP_NO_HISTORY | SP_FULL_ROLLOUT)) return SP_EINVAL;
   if (!KQV || !ctx || !img_off || !kept_off || !kept_cnt || !ws) return SP_EINVAL;
   if (G > 0 && (!grp_off || !grp_img || !grp_cap || !kept_idx)) return SP_EINVAL;
   if ((flags & SP_TRACE) && trace_steps > 0 && !trace) return SP_EINVAL;
   if (b_stop != b_stop) return SP_EINVAL;   // NaN
+  if (traj) {
+    if (!(traj->tau > 0.0f) || !(traj->beta > 0.0f && traj->beta <= 1.0f)) return SP_EINVAL;
+    if (traj->pstop_steps < 0 || (traj->pstop_steps > 0 && !traj->pstop)) return SP_EINVAL;
+    if ((G > 0 && !traj->kbar) || (T_vis > 0 && !traj->s)) return SP_EINVAL;
+    if (g != 1) return SP_EUNSUPPORTED;
+  }
   if (!aligned16(KQV) || !aligned16(ctx) || !aligned16(ws)) return SP_EINVAL;
   const SelectWs lay = select_ws_layout(dims, B, G, max_group, max_cap);
   if (ws_bytes < lay.total) return SP_EWORKSPACE;
@@ -162,6 +174,12 @@ sp_status stepprune_select(const sp_dims* dims, const void* KQV, const float* ct
   a.grp_cnt = grp_cnt;
   a.trace = trace;
   a.trace_steps = trace_steps;
+  a.traj_tau = traj ? traj->tau : 0.0f;
+  a.traj_beta = traj ? traj->beta : 0.0f;
+  a.traj_s = traj ? traj->s : nullptr;
+  a.traj_kbar = traj ? traj->kbar : nullptr;
+  a.traj_pstop = traj && traj->pstop_steps > 0 ? traj->pstop : nullptr;
+  a.traj_pstop_steps = traj && traj->pstop ? traj->pstop_steps : 0;
   a.gram = reinterpret_cast<float*>(wsb + lay.gram);
   a.gram_group_stride = lay.gstride;
   a.gram_ld = lay.gram_ld;
@@ -171,6 +189,39 @@ sp_status stepprune_select(const sp_dims* dims, const void* KQV, const float* ct
   a.err = reinterpret_cast<int32_t*>(wsb);
   a.events = events;
   return hip_status(launch_select(a, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+sp_status stepprune_select(const sp_dims* dims, const void* KQV, const float* ctx, int64_t T_vis,
+                           const int32_t* img_off, int32_t B, const int32_t* grp_off,
+                           const int32_t* grp_img, const int32_t* grp_cap, int32_t G,
+                           int32_t max_group, int32_t max_cap, const int32_t* kept_off,
+                           float b_stop, int32_t g, uint32_t flags, int32_t* kept_idx,
+                           int32_t* kept_cnt, int32_t* grp_cnt, float* trace, int32_t trace_steps,
+                           void* ws, size_t ws_bytes, const hipEvent_t* events,
+                           hipStream_t stream) {
+  return select_impl(dims, KQV, ctx, T_vis, img_off, B, grp_off, grp_img, grp_cap, G, max_group,
+                     max_cap, kept_off, b_stop, g, flags, kept_idx, kept_cnt, grp_cnt, trace,
+                     trace_steps, nullptr, ws, ws_bytes, events, stream);
+}
+
+sp_status stepprune_select_trajectory(const sp_dims* dims, const void* KQV, const float* ctx,
+                                      int64_t T_vis, const int32_t* img_off, int32_t B,
+                                      const int32_t* grp_off, const int32_t* grp_img,
+                                      const int32_t* grp_cap, int32_t G, int32_t max_group,
+                                      int32_t max_cap, const int32_t* kept_off, float b_stop,
+                                      int32_t g, uint32_t flags, int32_t* kept_idx,
+                                      int32_t* kept_cnt, int32_t* grp_cnt, float* trace,
+                                      int32_t trace_steps, const sp_trajectory* traj, void* ws,
+                                      size_t ws_bytes, const hipEvent_t* events,
+                                      hipStream_t stream) {
+  if (!traj) return SP_EINVAL;
+  return select_impl(dims, KQV, ctx, T_vis, img_off, B, grp_off, grp_img, grp_cap, G, max_group,
+                     max_cap, kept_off, b_stop, g, flags, kept_idx, kept_cnt, grp_cnt, trace,
+                     trace_steps, traj, ws, ws_bytes, events, stream);
 }
 
 sp_status stepprune_compact(const sp_dims* dims, const void* X, const int32_t* img_off,

@@ -56,6 +56,13 @@ struct SelParams {
   int32_t* grp_cnt_out;
   float* trace;
   int trace_steps;
+  // trajectory sums (Eqs. 5-7; traced g = 1 kernels, when traj_s is set)
+  float* traj_s;
+  float* traj_kbar;
+  float* traj_pstop;
+  int traj_pstop_steps;
+  float traj_c;        // log2(e) / tau
+  float traj_beta;
   int32_t* err;
 };
 
@@ -74,8 +81,9 @@ struct SelParams {
 //   ckeys [16][kGMax + 1]   grouped rounds: each wave's best keys, descending (slots
 //                           a launch never writes stay zero)
 //   ranked [16][kGMax + 1]  grouped rounds: each wave's copy of the merged ranks
+//   zpart [2][16]           trajectory sums: per-wave partial softmax sums by step parity
 struct SelLds {
-  int hmain, hsec, alpha, sm, hcol, shist, key, red, cnt, ckeys, ranked, total;
+  int hmain, hsec, alpha, sm, hcol, shist, key, red, cnt, ckeys, ranked, zpart, total;
   __host__ __device__ SelLds(int W, int lt, int ks, int alpha_ld, int hcap) {
     hmain = 0;
     hsec = hmain + 64 * W * lt * 4;
@@ -88,7 +96,8 @@ struct SelLds {
     cnt = red + 16 * 16;
     ckeys = cnt + 16 * 4;
     ranked = ckeys + 16 * (kGMax + 1) * 8;
-    total = ranked + 16 * (kGMax + 1) * 8;
+    zpart = ranked + 16 * (kGMax + 1) * 8;
+    total = zpart + 2 * 16 * 4;
   }
 };
 
@@ -233,6 +242,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     }
   }
   const bool no_history = (p.flags & SP_NO_HISTORY) != 0;
+  const bool full = (p.flags & SP_FULL_ROLLOUT) != 0;   // STOP scored, never taken while tokens remain
   const int lt = p.lt, ks = p.ks;
   const SelLds L(W, lt, ks, p.alpha_ld, p.hcap);
   float* hmain = reinterpret_cast<float*>(smem + L.hmain);
@@ -244,6 +254,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   unsigned long long* key = reinterpret_cast<unsigned long long*>(smem + L.key);
   unsigned long long* ckeys = reinterpret_cast<unsigned long long*>(smem + L.ckeys);
   unsigned long long* ranked = reinterpret_cast<unsigned long long*>(smem + L.ranked);
+  float* zpart = reinterpret_cast<float*>(smem + L.zpart);
   float4* red = reinterpret_cast<float4*>(smem + L.red);
   int* cnt = reinterpret_cast<int*>(smem + L.cnt);
 
@@ -611,8 +622,36 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   bool selected = false, sel_sec = false;
   int kept = 0;
 
+  // Trajectory sums (g = 1, traced kernels): step t's unnormalised candidate
+  // weights e = exp((l - max) / tau) stay in registers while the per-wave
+  // partial sums cross the step's closing barrier; at the top of step t + 1
+  // every lane adds the partials in wave order, and with p_t = e / Z updates
+  // s (its columns), K_bar and A.  Uniform values are kept in every lane.
+  const bool traj = TRACE && !GROUPED && p.traj_s != nullptr;
+  float tj_A = 1.0f, tj_bt = 1.0f, tj_kbar = 0.0f, tj_s = 0.0f, tj_s2 = 0.0f;
+  float tj_e = 0.0f, tj_e2 = 0.0f, tj_estop = 0.0f;
+  int tj_t = 0;
+  bool tj_pending = false;
+  auto traj_finish = [&]() {
+    const int pp = tj_t & 1;
+    float Z = tj_estop;
+    for (int w = 0; w < W; ++w) Z += zpart[pp * 16 + w];
+    const float inv = Z > 0.0f ? 1.0f / Z : 0.0f;
+    const float pst = Z > 0.0f ? tj_estop * inv : 1.0f;   // no finite candidate: p(STOP) = 1
+    tj_bt *= p.traj_beta;                                   // beta^t
+    const float wgt = tj_A * tj_bt * inv;
+    tj_s = fmaf(wgt, tj_e, tj_s);
+    tj_s2 = fmaf(wgt, tj_e2, tj_s2);
+    tj_kbar = fmaf(tj_A, 1.0f - pst, tj_kbar);
+    if (tid == 0 && p.traj_pstop && tj_t <= p.traj_pstop_steps)
+      p.traj_pstop[(int64_t)g * p.traj_pstop_steps + (tj_t - 1)] = pst;
+    tj_A *= 1.0f - pst;
+    tj_pending = false;
+  };
+
   for (int t = 1; t <= cap; ++t) {
     const int par = t & 1;
+    if (traj && tj_pending) traj_finish();
     const float inv = sm[0], st = sm[1];
     const float e_new = GROUPED ? 0.0f : sm[2];
 
@@ -844,7 +883,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
       }
       // STOP ends the episode only as the round's largest logit (it loses ties)
       const unsigned long long stop_key = l_stop > -INFINITY ? cand_key(l_stop, n) : 0ull;
-      const bool stop = top0 == 0ull || stop_key > top0;
+      const bool stop = top0 == 0ull || (!full && stop_key > top0);
       if (TRACE && tid == 0 && t <= p.trace_steps) {
         const int tw = gsz + 3;
         float* rec = p.trace + ((int64_t)g * p.trace_steps + (t - 1)) * tw;
@@ -881,7 +920,8 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
         else if (SEC) i1 = 512 + (wave << 4) + ((__ffsll((unsigned long long)__ballot(ls == vmax)) - 1) >> 2);
         if (lane == 0) atomicMax(&key[par], (unsigned long long)cand_key(vmax, i1));
       }
-      if (tid == 0 && l_stop > -INFINITY) atomicMax(&key[par], (unsigned long long)cand_key(l_stop, n));
+      if (tid == 0 && l_stop > -INFINITY && !full)
+        atomicMax(&key[par], (unsigned long long)cand_key(l_stop, n));
       if (TRACE) {
         // runner-up of this wave: the best candidate other than i1
         const float w1 = valid && j != i1 ? lj : -INFINITY;
@@ -908,6 +948,19 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
         rec[2] = r2;
         rec[3] = l_stop;
       }
+      if (traj) {
+        // this step's candidate weights (the taken token is still a candidate)
+        const float top = kk ? key_value(kk) : -INFINITY;
+        const float M = top > l_stop ? top : l_stop;
+        const bool any = M > -INFINITY;
+        tj_e = any && mcol && !selected ? __builtin_amdgcn_exp2f((lj - M) * p.traj_c) : 0.0f;
+        tj_e2 = any && ls > -INFINITY && sq == 0 ? __builtin_amdgcn_exp2f((ls - M) * p.traj_c) : 0.0f;
+        tj_estop = any && l_stop > -INFINITY ? __builtin_amdgcn_exp2f((l_stop - M) * p.traj_c) : 0.0f;
+        const float part = wave_sum_fused(tj_e + tj_e2);
+        if (lane == 0) zpart[par * 16 + wave] = part;
+        tj_t = t;
+        tj_pending = true;
+      }
       if (a == n) break;
       ++kept;
       if (j == a) selected = true;
@@ -924,6 +977,12 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   // bits, lane-owned columns first, then the second columns (one lane of each
   // quad reports; waves 0-3 hold them in ascending order).
   __syncthreads();
+  if (traj) {
+    if (tj_pending) traj_finish();
+    if (mcol) p.traj_s[g0 + j] = tj_s;
+    if (SEC && scol && sq == 0) p.traj_s[g0 + js] = tj_s2;
+    if (tid == 0) p.traj_kbar[g] = tj_kbar;
+  }
   const uint64_t ballot = __ballot(mcol && selected);
   const uint64_t sb = __ballot(scol && sel_sec && sq == 0);
   if (lane == 0) {
@@ -950,6 +1009,12 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     p.grp_count[g] = kept;
     if (p.grp_cnt_out) p.grp_cnt_out[g] = kept;
   }
+}
+
+// p_t(STOP) records past an episode's end hold NaN.
+__global__ void fill_nan_kernel(float* x, int64_t count) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < count) x[i] = __int_as_float(0x7fc00000);
 }
 
 // Trace records (width floats) past an episode's end carry taken = -2.
@@ -1110,6 +1175,18 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.grp_cnt_out = a.grp_cnt;
   p.trace = trace ? a.trace : nullptr;
   p.trace_steps = trace ? a.trace_steps : 0;
+  const bool traj = a.traj_s != nullptr;
+  p.traj_s = a.traj_s;
+  p.traj_kbar = a.traj_kbar;
+  p.traj_pstop = a.traj_pstop;
+  p.traj_pstop_steps = a.traj_pstop ? a.traj_pstop_steps : 0;
+  p.traj_c = traj ? 1.4426950408889634f / a.traj_tau : 0.0f;
+  p.traj_beta = a.traj_beta;
+  if (traj && p.traj_pstop_steps > 0) {
+    const int64_t count = (int64_t)a.G * p.traj_pstop_steps;
+    hipLaunchKernelGGL(fill_nan_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, stream,
+                       p.traj_pstop, count);
+  }
   p.err = a.err;
 
   // Waves: one lane per token column up to 512 columns (2 waves per SIMD, 256
@@ -1169,7 +1246,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   const void* fn = nullptr;
 #define SP_PICK(RR, SEC, MAXT)                                                           \
   if (!grouped && rreg == RR && sec == SEC && (MAXT == 1024) == wide)                    \
-    fn = trace ? (const void*)select_kernel<RR, SEC, true, MAXT, 1>                      \
+    fn = trace || traj ? (const void*)select_kernel<RR, SEC, true, MAXT, 1>              \
                : (const void*)select_kernel<RR, SEC, false, MAXT, 1>;
   SP_PICK(64, false, 512) SP_PICK(128, false, 512) SP_PICK(160, false, 512)
   SP_PICK(64, true, 512) SP_PICK(128, true, 512) SP_PICK(160, true, 512)

@@ -108,6 +108,13 @@ struct SelectArgs {
   int32_t* grp_cnt;
   float* trace;
   int trace_steps;
+  // trajectory sums (Eqs. 5-7), all null / zero when not requested
+  float traj_tau;
+  float traj_beta;
+  float* traj_s;         // [T_vis]
+  float* traj_kbar;      // [G]
+  float* traj_pstop;     // [G, traj_pstop_steps] or null
+  int traj_pstop_steps;
   // workspace pieces
   float* gram;
   int64_t gram_group_stride;

@@ -74,7 +74,8 @@ def _close(a: float, b: float, tol: float) -> bool:
 
 def check_selection(KQV: np.ndarray, ctx: np.ndarray, grp_off, grp_img, caps, b_stop: float, h: int,
                     actions: Sequence[Sequence[int]], trace: Optional[np.ndarray], dtype: str,
-                    no_history: bool = False, groups: Optional[Sequence[int]] = None) -> SelectReport:
+                    no_history: bool = False, groups: Optional[Sequence[int]] = None,
+                    ignore_stop: bool = False) -> SelectReport:
     """Staged, teacher-forced check of every episode in ``groups``.
 
     ``actions[g]`` is the GPU's taken-candidate sequence of group g (token index,
@@ -95,7 +96,7 @@ def check_selection(KQV: np.ndarray, ctx: np.ndarray, grp_off, grp_img, caps, b_
         c = ctx[int(grp_img[g])]
         args = (Kall[r0:r1], Qall[r0:r1], Vall[r0:r1], start, k_stop, c, cap, b_stop, h)
         forced = [STOP if a == -1 else a for a in seq]
-        ep = oracle.run_episode(*args, no_history=no_history, forced=forced)
+        ep = oracle.run_episode(*args, no_history=no_history, forced=forced, ignore_stop=ignore_stop)
         rep.episodes += 1
         where = f"group {g} (n={n}, cap={cap})"
         assert len(ep.steps) == len(seq), f"{where}: oracle replay took {len(ep.steps)} steps, GPU {len(seq)}"
@@ -130,7 +131,8 @@ def check_selection(KQV: np.ndarray, ctx: np.ndarray, grp_off, grp_img, caps, b_
                     f"{where} step {t + 1}: top-2 {pair_gpu} vs {pair_or}")
                 rep.max_logit_err = max(rep.max_logit_err, err / scale)
         if exempt_here == 0:
-            free = oracle.run_episode(*args, no_history=no_history, keep_steps=False)
+            free = oracle.run_episode(*args, no_history=no_history, keep_steps=False,
+                                      ignore_stop=ignore_stop)
             rep.free_running_checked += 1
             gpu_sel = [a for a in seq if a != -1]
             assert free.actions == gpu_sel, f"{where}: free-running oracle differs without near-ties"
@@ -229,4 +231,64 @@ def check_grouped_selection(KQV: np.ndarray, ctx: np.ndarray, grp_off, grp_img, 
             assert [sorted(x) for x in free.groups] == [sorted(x) for x in seq if x != [-1]], (
                 f"{where}: free-running oracle differs without near-ties")
             rep.free_running_equal += 1
+    return rep
+
+
+TRAJ_TOL = 1e-4
+
+
+@dataclass
+class TrajectoryReport:
+    episodes: int = 0
+    max_s_err: float = 0.0
+    max_kbar_err: float = 0.0
+    max_pstop_err: float = 0.0
+
+
+def check_trajectory(KQV: np.ndarray, ctx: np.ndarray, grp_off, grp_img, caps, b_stop: float,
+                     h: int, actions: Sequence[Sequence[int]], s_gpu: np.ndarray,
+                     kbar_gpu: np.ndarray, pstop_gpu: Optional[np.ndarray], tau: float,
+                     beta: float, ignore_stop: bool = False, no_history: bool = False,
+                     groups: Optional[Sequence[int]] = None) -> TrajectoryReport:
+    """The trajectory sums of Eqs. 5-7 against the oracle, staged and
+    teacher-forced like check_selection: the oracle replays the GPU's actions
+    on the GPU's projected rows, so both sides sum over the same steps.
+
+    Tolerance TRAJ_TOL = 1e-4: per group the normwise relative error of s, the
+    error of K_bar relative to max(1, K_bar), and the absolute error of every
+    p_t(STOP).  Staged logits agree to about 1e-6 of their scale (float32
+    against float64), and p_t moves by |dl| / tau, so for tau >= 0.5 and logit
+    scales up to ~20 the error stays an order of magnitude below the bar."""
+    rep = TrajectoryReport()
+    T_vis = KQV.shape[0] - 2
+    Kall, Qall, Vall = KQV[:, :h], KQV[:, h:2 * h], KQV[:, 2 * h:3 * h]
+    start = (Kall[T_vis], Qall[T_vis], Vall[T_vis])
+    k_stop = Kall[T_vis + 1]
+    gs = range(len(grp_img)) if groups is None else groups
+    for g in gs:
+        r0, r1 = int(grp_off[g]), int(grp_off[g + 1])
+        n = r1 - r0
+        forced = [STOP if a == -1 else a for a in actions[g]]
+        tr = oracle.run_trajectory(Kall[r0:r1], Qall[r0:r1], Vall[r0:r1], start, k_stop,
+                                   ctx[int(grp_img[g])], int(caps[g]), b_stop, h, tau, beta,
+                                   ignore_stop=ignore_stop, no_history=no_history, forced=forced)
+        where = f"group {g} (n={n})"
+        assert len(tr.pstop) == len(forced), f"{where}: replay length"
+        got = np.asarray(s_gpu[r0:r1], np.float64)
+        den = max(float(np.linalg.norm(tr.s)), 1e-30)
+        e_s = float(np.linalg.norm(got - tr.s)) / den if n else 0.0
+        assert e_s <= TRAJ_TOL, f"{where}: s relative error {e_s:.3e}"
+        e_k = abs(float(kbar_gpu[g]) - tr.kbar) / max(1.0, tr.kbar)
+        assert e_k <= TRAJ_TOL, f"{where}: K_bar {float(kbar_gpu[g])!r} vs {tr.kbar!r}"
+        if pstop_gpu is not None:
+            row = np.asarray(pstop_gpu[g], np.float64)
+            steps = len(tr.pstop)
+            if steps:
+                e_p = float(np.abs(row[:steps] - np.asarray(tr.pstop)).max())
+                assert e_p <= TRAJ_TOL, f"{where}: p(STOP) error {e_p:.3e}"
+                rep.max_pstop_err = max(rep.max_pstop_err, e_p)
+            assert np.isnan(row[steps:]).all(), f"{where}: p(STOP) past the end"
+        rep.episodes += 1
+        rep.max_s_err = max(rep.max_s_err, e_s)
+        rep.max_kbar_err = max(rep.max_kbar_err, e_k)
     return rep

@@ -100,6 +100,32 @@ def test_select_validation(sp):
     assert _select(sp) == sp.SP_EWORKSPACE
 
 
+def _select_traj(sp, traj, **kw):
+    args = dict(KQV=FAKE, ctx=FAKE, T_vis=10, img_off=FAKE, B=1, grp_off=FAKE, grp_img=FAKE,
+                grp_cap=FAKE, G=1, max_group=10, max_cap=4, kept_off=FAKE, b_stop=0.0, g=1,
+                flags=0, kept_idx=FAKE, kept_cnt=FAKE, grp_cnt=None, trace=None, trace_steps=0,
+                traj=traj, ws=FAKE, ws_bytes=0)
+    args.update(kw)
+    return sp.stepprune_select_trajectory(_dims(sp), stream=0, raise_on_error=False, **args)
+
+
+def test_select_trajectory_validation(sp):
+    ok = sp.trajectory(1.0, 0.9, FAKE, FAKE)
+    assert _select_traj(sp, ok) == sp.SP_EWORKSPACE                    # accepted up to the workspace
+    assert _select_traj(sp, None) == sp.SP_EINVAL
+    assert _select_traj(sp, sp.trajectory(0.0, 0.9, FAKE, FAKE)) == sp.SP_EINVAL      # tau <= 0
+    assert _select_traj(sp, sp.trajectory(1.0, 0.0, FAKE, FAKE)) == sp.SP_EINVAL      # beta <= 0
+    assert _select_traj(sp, sp.trajectory(1.0, 1.5, FAKE, FAKE)) == sp.SP_EINVAL      # beta > 1
+    assert _select_traj(sp, sp.trajectory(1.0, 0.9, None, FAKE)) == sp.SP_EINVAL
+    assert _select_traj(sp, sp.trajectory(1.0, 0.9, FAKE, None)) == sp.SP_EINVAL
+    assert _select_traj(sp, sp.trajectory(1.0, 0.9, FAKE, FAKE, None, 3)) == sp.SP_EINVAL
+    assert _select_traj(sp, ok, g=2) == sp.SP_EUNSUPPORTED
+    assert _select_traj(sp, ok, flags=sp.SP_FULL_ROLLOUT | sp.SP_TRACE, trace=FAKE,
+                        trace_steps=3) == sp.SP_EWORKSPACE
+    assert _select(sp, flags=sp.SP_FULL_ROLLOUT) == sp.SP_EWORKSPACE
+    assert _select(sp, flags=8) == sp.SP_EINVAL
+
+
 def _compact(sp, dm=None, **kw):
     args = dict(X=FAKE, img_off=FAKE, E_text=FAKE, text_off=FAKE, kept_idx=FAKE, kept_off=FAKE,
                 kept_cnt=FAKE, B=2, layout=sp.SP_LAYOUT_PADDED, rows_per_image=8, out_rows=16,
