@@ -180,6 +180,48 @@ def hbm_traffic(kernel, workload):
     return float(rec["bytes_per_launch"])
 
 
+def trajectory_pass(run, tb, K, hip):
+    """Select-stage time with the trajectory sums over the full rollout, beside
+    the plain selection and the plain full rollout (g = 1 workloads), single
+    stream, HIP events around each call."""
+    import numpy as np
+    import torch
+    from paper_2609_13804_amd import binding as sp
+    tau, beta = tb
+    stream = torch.cuda.current_stream().cuda_stream
+    outs = run.trajectory_outputs()
+    variants = {
+        "plain_select_us": lambda e: run.select(stream, flags=0, events=e),
+        "full_rollout_select_us": lambda e: run.select(stream, flags=sp.SP_FULL_ROLLOUT, events=e),
+        "traced_full_rollout_select_us": lambda e: run.select(
+            stream, flags=sp.SP_FULL_ROLLOUT | (sp.SP_TRACE if run.trace is not None else 0),
+            events=e),
+        "trajectory_select_us": lambda e: run.select_trajectory(tau, beta, flags=sp.SP_FULL_ROLLOUT,
+                                                                stream=stream, out=outs, events=e),
+    }
+    res = {"tau": tau, "beta": beta, "rollout": "full (SP_FULL_ROLLOUT)"}
+    for name, fn in variants.items():
+        for _ in range(3):
+            fn(None)
+        torch.cuda.synchronize()
+        evs = [[hip.create() for _ in range(6)] for _ in range(K)]
+        for e in evs:
+            hip.record(e[0], stream)
+            fn([e[1], e[2], e[3], e[4]])
+            hip.record(e[5], stream)
+        torch.cuda.synchronize()
+        res[name] = round(float(np.mean([1e3 * hip.ms(e[0], e[5]) for e in evs])), 2)
+        res[name.replace("select_us", "recurrence_us")] = round(
+            float(np.mean([1e3 * hip.ms(e[3], e[4]) for e in evs])), 2)
+        for e in evs:
+            for ev in e:
+                hip.destroy(ev)
+    if any(run.device_errors()):
+        raise RuntimeError(f"device error words {run.device_errors()}")
+    res["kbar_mean"] = round(float(outs[1][:run.sizes.G].mean()), 4)
+    return res
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -194,6 +236,9 @@ def main(argv=None):
     ap.add_argument("--schedule", choices=["staggered", "rr"], default="staggered",
                     help="pipelined pass: projections on one stream ahead of per-slot select "
                          "streams (staggered), or whole batches round-robin (rr)")
+    ap.add_argument("--trajectory", type=float, nargs=2, metavar=("TAU", "BETA"), default=None,
+                    help="also time the selection with the trajectory sums of Eqs. 5-7 over the "
+                         "full rollout (stepprune_select_trajectory) against the plain selection")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle work for the CPU baseline sample")
@@ -224,8 +269,10 @@ def main(argv=None):
     lay = W.make_layout(w)
     b_stop = W.stop_bias(w)
     inp = W.make_inputs(w)
-    run = DeviceRun(w, inp, lay, b_stop)
-    del inp
+    run = DeviceRun(w, inp, lay, b_stop,
+                    trace_steps=int(lay.grp_cap.max()) + 1 if args.trajectory is not None else 0)
+    run.flags = 0      # the timed passes run the untraced kernels (a trace buffer is only
+    del inp            # allocated for the traced variant of --trajectory)
     stream = torch.cuda.current_stream().cuda_stream
     hip = HipEvents()
 
@@ -408,6 +455,8 @@ def main(argv=None):
         "selection_steps_per_s": round(sum(steps_g) / (stages["select"] * 1e-6), 1),
         "roofline": roofline,
     }
+    if args.trajectory is not None:
+        out["trajectory"] = trajectory_pass(run, args.trajectory, K, hip)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, lay, b_stop, args.cpu_budget)
         one = cpu_baseline(w, lay, b_stop, args.cpu_budget * 0.5, single_thread=True)

@@ -220,8 +220,9 @@ typedef struct {
  * stepprune_select, and along the same trajectory the sums described with
  * sp_trajectory (Eqs. 5-7).  Arguments as for stepprune_select plus `traj`
  * (host pointer, required).  g must be 1 (SP_EUNSUPPORTED otherwise);
- * tau <= 0, beta outside (0, 1] or a NULL s / kbar give SP_EINVAL.  Runs the
- * traced selection kernel, so it is slower than stepprune_select.
+ * tau <= 0, beta outside (0, 1] or a NULL s / kbar give SP_EINVAL.  Runs a
+ * selection kernel built with the sums (one exp per candidate and a wave sum
+ * per step); it takes the same decisions as stepprune_select.
  */
 sp_status stepprune_select_trajectory(const sp_dims* dims,
                                       const void* KQV, const float* ctx, int64_t T_vis,

@@ -56,7 +56,7 @@ struct SelParams {
   int32_t* grp_cnt_out;
   float* trace;
   int trace_steps;
-  // trajectory sums (Eqs. 5-7; traced g = 1 kernels, when traj_s is set)
+  // trajectory sums (Eqs. 5-7; g = 1 kernels instantiated with TRAJ)
   float* traj_s;
   float* traj_kbar;
   float* traj_pstop;
@@ -209,7 +209,7 @@ __device__ __forceinline__ int key_index(uint64_t k) {
 // its g best candidates, writes their keys to LDS, and after the barrier
 // every wave ranks all of them the same way, stops if STOP's key beats the
 // best, and otherwise takes the g best as the round's group.
-template <int RREG, bool SEC, bool TRACE, int MAXT, int GMAX>
+template <int RREG, bool SEC, bool TRACE, int MAXT, int GMAX, bool TRAJ>
 __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   constexpr bool GROUPED = GMAX > 1;
   static_assert(GMAX >= 1 && GMAX <= kGMax, "group size");
@@ -622,12 +622,12 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   bool selected = false, sel_sec = false;
   int kept = 0;
 
-  // Trajectory sums (g = 1, traced kernels): step t's unnormalised candidate
+  // Trajectory sums (g = 1, TRAJ kernels): step t's unnormalised candidate
   // weights e = exp((l - max) / tau) stay in registers while the per-wave
   // partial sums cross the step's closing barrier; at the top of step t + 1
   // every lane adds the partials in wave order, and with p_t = e / Z updates
   // s (its columns), K_bar and A.  Uniform values are kept in every lane.
-  const bool traj = TRACE && !GROUPED && p.traj_s != nullptr;
+  const bool traj = TRAJ && !GROUPED && p.traj_s != nullptr;
   float tj_A = 1.0f, tj_bt = 1.0f, tj_kbar = 0.0f, tj_s = 0.0f, tj_s2 = 0.0f;
   float tj_e = 0.0f, tj_e2 = 0.0f, tj_estop = 0.0f;
   int tj_t = 0;
@@ -1209,6 +1209,8 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   // grouped kernels hold the newest group's values too, and their histories
   // grow g entries a round: 64 history registers, then the LDS tier
   int rreg = wide ? 32 : need <= 64 || grouped ? 64 : need <= 128 ? 128 : 160;
+  // the trajectory sums take registers too: at most 128 history registers
+  if (a.traj_s && rreg > 128) rreg = 128;
   p.W = W;
   p.hcap = (int)align_up((size_t)need + 1, 4);
   // alpha covers the register blocks' prefetch (up to rreg) and the second
@@ -1245,17 +1247,27 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
 
   const void* fn = nullptr;
 #define SP_PICK(RR, SEC, MAXT)                                                           \
-  if (!grouped && rreg == RR && sec == SEC && (MAXT == 1024) == wide)                    \
-    fn = trace || traj ? (const void*)select_kernel<RR, SEC, true, MAXT, 1>              \
-               : (const void*)select_kernel<RR, SEC, false, MAXT, 1>;
-  SP_PICK(64, false, 512) SP_PICK(128, false, 512) SP_PICK(160, false, 512)
-  SP_PICK(64, true, 512) SP_PICK(128, true, 512) SP_PICK(160, true, 512)
+  if (!grouped && rreg == RR && sec == SEC && (MAXT == 1024) == wide) {                  \
+    if (traj)                                                                            \
+      fn = trace ? (const void*)select_kernel<RR, SEC, true, MAXT, 1, true>              \
+                 : (const void*)select_kernel<RR, SEC, false, MAXT, 1, true>;            \
+    else                                                                                 \
+      fn = trace ? (const void*)select_kernel<RR, SEC, true, MAXT, 1, false>             \
+                 : (const void*)select_kernel<RR, SEC, false, MAXT, 1, false>;           \
+  }
+#define SP_PICK_NT(RR, SEC, MAXT)                                                        \
+  if (!grouped && rreg == RR && sec == SEC && (MAXT == 1024) == wide && !traj)           \
+    fn = trace ? (const void*)select_kernel<RR, SEC, true, MAXT, 1, false>               \
+               : (const void*)select_kernel<RR, SEC, false, MAXT, 1, false>;
+  SP_PICK(64, false, 512) SP_PICK(128, false, 512) SP_PICK_NT(160, false, 512)
+  SP_PICK(64, true, 512) SP_PICK(128, true, 512) SP_PICK_NT(160, true, 512)
   SP_PICK(32, false, 1024)
 #undef SP_PICK
+#undef SP_PICK_NT
 #define SP_PICK_G(RR, SEC, MAXT)                                                         \
   if (grouped && rreg == RR && sec == SEC && (MAXT == 1024) == wide)                     \
-    fn = trace ? (const void*)select_kernel<RR, SEC, true, MAXT, kGMax>                  \
-               : (const void*)select_kernel<RR, SEC, false, MAXT, kGMax>;
+    fn = trace ? (const void*)select_kernel<RR, SEC, true, MAXT, kGMax, false>           \
+               : (const void*)select_kernel<RR, SEC, false, MAXT, kGMax, false>;
   SP_PICK_G(64, false, 512) SP_PICK_G(64, true, 512) SP_PICK_G(32, false, 1024)
 #undef SP_PICK_G
   if (!fn) return hipErrorInvalidValue;

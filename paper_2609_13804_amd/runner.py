@@ -133,22 +133,30 @@ class DeviceRun:
                                    self.kept_cnt, self.grp_cnt, self.trace, self.trace_steps,
                                    self.ws[1], self.ws_bytes[1], stream, events=events)
 
-    def select_trajectory(self, tau: float, beta: float, flags: Optional[int] = None,
-                          pstop_steps: int = 0, stream=None):
-        """The selection and the trajectory sums of Eqs. 5-7 along it (g = 1);
-        returns (s [T_vis], kbar [G], pstop [G, pstop_steps] or None)."""
+    def trajectory_outputs(self, pstop_steps: int = 0):
+        """Buffers for select_trajectory: (s [T_vis], kbar [G], pstop [G, steps] or None)."""
         s_, dev = self.sizes, self.X.device
         ts = torch.zeros(max(1, s_.T_vis), dtype=torch.float32, device=dev)
         kb = torch.zeros(max(1, s_.G), dtype=torch.float32, device=dev)
         ps = (torch.empty((s_.G, pstop_steps), dtype=torch.float32, device=dev)
               if pstop_steps > 0 else None)
+        return ts, kb, ps
+
+    def select_trajectory(self, tau: float, beta: float, flags: Optional[int] = None,
+                          pstop_steps: int = 0, stream=None, out=None, events=None):
+        """The selection and the trajectory sums of Eqs. 5-7 along it (g = 1);
+        returns (s [T_vis], kbar [G], pstop [G, pstop_steps] or None), in
+        ``out`` (from trajectory_outputs) when given."""
+        s_ = self.sizes
+        ts, kb, ps = out if out is not None else self.trajectory_outputs(pstop_steps)
+        pstop_steps = 0 if ps is None else int(ps.shape[1])
         tj = sp.trajectory(tau, beta, ts, kb, ps, pstop_steps)
         sp.stepprune_select_trajectory(self.dims, self.KQV, self.ctx, s_.T_vis, self.img_off, s_.B,
                                        self.grp_off, self.grp_img, self.grp_cap, s_.G,
                                        s_.max_group, s_.max_cap, self.kept_off, self.b_stop, self.g,
                                        self.flags if flags is None else flags, self.kept_idx,
                                        self.kept_cnt, self.grp_cnt, self.trace, self.trace_steps, tj,
-                                       self.ws[1], self.ws_bytes[1], stream)
+                                       self.ws[1], self.ws_bytes[1], stream, events=events)
         return ts, kb, ps
 
     def compact(self, stream=None, events=None):
