@@ -233,9 +233,12 @@ def main(argv=None):
                          "or round-robin streams (rr); 1: no pipelined pass")
     ap.add_argument("--slots", type=int, default=4,
                     help="buffer slots of the staggered pipelined pass (batches in flight)")
-    ap.add_argument("--schedule", choices=["staggered", "rr"], default="staggered",
-                    help="pipelined pass: projections on one stream ahead of per-slot select "
-                         "streams (staggered), or whole batches round-robin (rr)")
+    ap.add_argument("--schedule", choices=["staggered", "staggered-gram", "rr"], default="staggered",
+                    help="pipelined pass: projections on one stream ahead of select (Gram "
+                         "products + recurrence) and compaction on per-slot streams "
+                         "(staggered), the Gram products on the projection stream too "
+                         "(staggered-gram: SP_GRAM_ONLY / SP_REUSE_GRAM), or whole batches "
+                         "round-robin (rr)")
     ap.add_argument("--trajectory", type=float, nargs=2, metavar=("TAU", "BETA"), default=None,
                     help="also time the selection with the trajectory sums of Eqs. 5-7 over the "
                          "full rollout (stepprune_select_trajectory) against the plain selection")
@@ -395,8 +398,9 @@ def main(argv=None):
     S = max(1, args.streams)
     if S > 1:
         from paper_2609_13804_amd.runner import Pipeline
-        if args.schedule == "staggered":
-            pipe = Pipeline(run, max(S, args.slots), min(S, Pipeline.MAX_STREAMS))
+        if args.schedule.startswith("staggered"):
+            pipe = Pipeline(run, max(S, args.slots), min(S, Pipeline.MAX_STREAMS),
+                            split_gram=args.schedule == "staggered-gram")
             runs = pipe.runs
             issue = lambda k: pipe.issue()
         else:
@@ -441,7 +445,7 @@ def main(argv=None):
         "data": "synthetic",
         "config": {"workload": w.name, "images": s.B, "groups": s.G, "streams": S,
                    "schedule": args.schedule if S > 1 else "single",
-                   "slots": max(S, args.slots) if S > 1 and args.schedule == "staggered" else S,
+                   "slots": max(S, args.slots) if S > 1 and args.schedule != "rr" else S,
                    "tokens": int(s.T_vis), "d": w.d, "h": w.h, "text_tokens": int(s.T_txt),
                    "layout": w.layout, "b_stop": b_stop, "tokens_per_round": w.g,
                    "kept_mean_per_image": round(float(kept_b.mean()), 3),

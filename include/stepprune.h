@@ -75,9 +75,16 @@ enum {
   SP_TRACE = 1u,       /* stepprune_select writes the per-step trace */
   SP_NO_HISTORY = 2u,  /* pointer query frozen at its first value (diagnostic:
                           the selector collapses to top-K of the first scores, Eq. 1) */
-  SP_FULL_ROLLOUT = 4u /* the rollout that the trajectory sums of Eqs. 5-7 run over:
+  SP_FULL_ROLLOUT = 4u,/* the rollout that the trajectory sums of Eqs. 5-7 run over:
                           STOP is scored but not taken while a token is left, so
                           every episode runs to its cap (or out of tokens) */
+  /* The two phases of stepprune_select, for callers that overlap batches:
+     SP_GRAM_ONLY computes the per-group Gram products (the matrix-core part)
+     into the workspace and returns; a later call with SP_REUSE_GRAM and the
+     same arguments and workspace runs the recurrence on them.  Between the
+     two, KQV, ctx, the offsets and the workspace must not change. */
+  SP_GRAM_ONLY = 8u,
+  SP_REUSE_GRAM = 16u
 };
 
 enum { SP_LAYOUT_PADDED = 0, SP_LAYOUT_PACKED = 1 };
@@ -161,7 +168,9 @@ sp_status stepprune_project(const sp_dims* dims,
  *  b_stop         additive STOP bias (may be +-inf)
  *  g              tokens kept per non-STOP round, 1 <= g <= 5
  *                 (SP_EUNSUPPORTED above 5)
- *  flags          SP_TRACE, SP_NO_HISTORY, SP_FULL_ROLLOUT
+ *  flags          SP_TRACE, SP_NO_HISTORY, SP_FULL_ROLLOUT, SP_GRAM_ONLY or
+ *                 SP_REUSE_GRAM (not both; SP_GRAM_ONLY writes none of the
+ *                 outputs and is refused by stepprune_select_trajectory)
  *  kept_idx  out  image-local kept indices, ascending per image, at kept_off[b]
  *  kept_cnt  out  [B] kept count per image (0 for an image whose slice of
  *                 kept_idx overflows, with SP_DEV_OUTPUT_OVERFLOW)

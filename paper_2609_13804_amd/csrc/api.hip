@@ -135,7 +135,10 @@ sp_status select_impl(const sp_dims* dims, const void* KQV, const float* ctx, in
   if (g < 1) return SP_EINVAL;
   if (g > kGMax) return SP_EUNSUPPORTED;
   if (max_group > kMaxGroup) return SP_EUNSUPPORTED;
-  if (flags & ~(uint32_t)(SP_TRACE | SP_NO_HISTORY | SP_FULL_ROLLOUT)) return SP_EINVAL;
+  if (flags & ~(uint32_t)(SP_TRACE | SP_NO_HISTORY | SP_FULL_ROLLOUT | SP_GRAM_ONLY | SP_REUSE_GRAM))
+    return SP_EINVAL;
+  if ((flags & SP_GRAM_ONLY) && (flags & SP_REUSE_GRAM)) return SP_EINVAL;
+  if ((flags & SP_GRAM_ONLY) && traj) return SP_EINVAL;
   if (!KQV || !ctx || !img_off || !kept_off || !kept_cnt || !ws) return SP_EINVAL;
   if (G > 0 && (!grp_off || !grp_img || !grp_cap || !kept_idx)) return SP_EINVAL;
   if ((flags & SP_TRACE) && trace_steps > 0 && !trace) return SP_EINVAL;

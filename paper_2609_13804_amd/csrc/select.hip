@@ -1120,7 +1120,10 @@ __global__ __launch_bounds__(64) void finalize_kernel(const int32_t* __restrict_
 }  // namespace
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
+  const bool gram_only = (a.flags & SP_GRAM_ONLY) != 0;
+  const bool reuse_gram = (a.flags & SP_REUSE_GRAM) != 0;
   if (a.G == 0) {
+    if (gram_only) return hipSuccess;
     if (a.B > 0)
       hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(64), 0, stream, a.img_off, a.B,
                          a.grp_off, a.grp_img, a.G, a.grp_kept, a.grp_count, a.max_cap, a.kept_off,
@@ -1144,9 +1147,11 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   ga.gram_group_stride = a.gram_group_stride;
   ga.gram_ld = a.gram_ld;
   ga.err = a.err;
-  hipError_t e = launch_gram_gemm(ga, stream);
+  // the Gram products, unless a previous SP_GRAM_ONLY call left them in ws
+  hipError_t e = reuse_gram ? hipSuccess : launch_gram_gemm(ga, stream);
   if (e != hipSuccess) return e;
   record_event(a.events, 1, stream);
+  if (gram_only) return hipGetLastError();
 
   const bool trace = (a.flags & SP_TRACE) && a.trace && a.trace_steps > 0;
   if (trace) {

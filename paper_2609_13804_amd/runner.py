@@ -204,28 +204,32 @@ class DeviceRun:
 
 
 class Pipeline:
-    """A stream of batches through the three stages with the projection of
-    later batches overlapping the selection of earlier ones.
+    """A stream of batches through the three stages with the matrix-core work
+    of later batches overlapping the recurrences of earlier ones.
 
     The recurrence of one batch occupies one compute unit per episode for
     most of a batch's time while the projection and Gram products need the
-    whole chip, so batches are staggered: every projection runs on one
-    stream, in batch order, and batch k's select + compact run on select
-    stream k mod ``streams``.  Batch k uses buffer slot k mod ``slots``, a
+    whole chip, so batches are staggered: batch k's projection runs on one
+    stream, in batch order, and its selection and compaction on select stream
+    k mod ``streams``.  With ``split_gram`` the selection's Gram products
+    (SP_GRAM_ONLY) join the projection stream and only the recurrence
+    (SP_REUSE_GRAM) runs on the select stream; measured on the 16 x 576 batch
+    this is slower (38K against 44K images/s): concurrent GEMMs of two
+    batches fill each other's last tile rounds.  Batch k uses buffer slot k mod ``slots``, a
     DeviceRun with its own outputs and workspaces (inputs shared read-only):
     a slot's projection waits for the slot's previous select + compact, and
-    its select waits for its projection.  More slots than select streams let
-    the projection run ahead of the recurrences.  All streams use the
+    its recurrence waits for its projection and Gram products.  More slots
+    than select streams let the GEMM stream run ahead.  All streams use the
     default priority.
 
-    The projections go to the caller's current stream, so the pipeline uses
+    The GEMM work goes to the caller's current stream, so the pipeline uses
     streams + 1 streams in all: at most three select streams keep every
     stream on a hardware queue of its own under HIP's default of four per
     process."""
 
     MAX_STREAMS = 3
 
-    def __init__(self, run: DeviceRun, slots: int = 4, streams: int = 3):
+    def __init__(self, run: DeviceRun, slots: int = 4, streams: int = 3, split_gram: bool = False):
         if not 1 <= streams <= self.MAX_STREAMS:
             raise ValueError(f"streams must be 1..{self.MAX_STREAMS}")
         if slots < streams:
@@ -235,6 +239,7 @@ class Pipeline:
         self.sel_streams = [torch.cuda.Stream() for _ in range(streams)]
         self.projected = [torch.cuda.Event() for _ in self.runs]
         self.done = [torch.cuda.Event() for _ in self.runs]
+        self.split_gram = split_gram
         self.k = 0
 
     def issue(self):
@@ -245,9 +250,11 @@ class Pipeline:
         if self.k >= len(self.runs):
             ps.wait_event(self.done[s])
         r.project(ps.cuda_stream)
+        if self.split_gram:
+            r.select(ps.cuda_stream, flags=r.flags | sp.SP_GRAM_ONLY)
         self.projected[s].record(ps)
         ss.wait_event(self.projected[s])
-        r.select(ss.cuda_stream)
+        r.select(ss.cuda_stream, flags=r.flags | (sp.SP_REUSE_GRAM if self.split_gram else 0))
         if r.out is not None:
             r.compact(ss.cuda_stream)
         self.done[s].record(ss)

@@ -90,7 +90,7 @@ def test_select_validation(sp):
     assert _select(sp, g=5) == sp.SP_EWORKSPACE                         # accepted up to the workspace
     assert _select(sp, max_group=1023) == sp.SP_EUNSUPPORTED
     assert _select(sp, max_group=-1) == sp.SP_EINVAL
-    assert _select(sp, flags=8) == sp.SP_EINVAL
+    assert _select(sp, flags=32) == sp.SP_EINVAL                        # unknown flag
     assert _select(sp, flags=sp.SP_TRACE, trace_steps=5, trace=None) == sp.SP_EINVAL
     assert _select(sp, b_stop=float("nan")) == sp.SP_EINVAL
     assert _select(sp, KQV=None) == sp.SP_EINVAL
@@ -123,7 +123,11 @@ def test_select_trajectory_validation(sp):
     assert _select_traj(sp, ok, flags=sp.SP_FULL_ROLLOUT | sp.SP_TRACE, trace=FAKE,
                         trace_steps=3) == sp.SP_EWORKSPACE
     assert _select(sp, flags=sp.SP_FULL_ROLLOUT) == sp.SP_EWORKSPACE
-    assert _select(sp, flags=8) == sp.SP_EINVAL
+    assert _select(sp, flags=sp.SP_GRAM_ONLY) == sp.SP_EWORKSPACE
+    assert _select(sp, flags=sp.SP_REUSE_GRAM) == sp.SP_EWORKSPACE
+    assert _select(sp, flags=sp.SP_GRAM_ONLY | sp.SP_REUSE_GRAM) == sp.SP_EINVAL
+    assert _select_traj(sp, ok, flags=sp.SP_GRAM_ONLY) == sp.SP_EINVAL
+    assert _select(sp, flags=32) == sp.SP_EINVAL                        # unknown flag
 
 
 def _compact(sp, dm=None, **kw):

@@ -102,6 +102,27 @@ def test_trace_and_plain_kernels_agree(gpu_lib, name):
         assert torch.equal(out1, run.out)
 
 
+@pytest.mark.parametrize("name", ["tiny_bf16", "small_packed_bf16"])
+def test_two_phase_selection_matches_one_call(gpu_lib, name):
+    """SP_GRAM_ONLY then SP_REUSE_GRAM (the pipeline's split) gives the one
+    call's kept lists and trace, bit for bit; the first phase writes no output."""
+    from paper_2609_13804_amd import binding as sp
+    w, inp, lay, run = _setup(name)
+    run.run()
+    torch.cuda.synchronize()
+    kept, tr = run.kept_lists(), run.trace.clone()
+    run.kept_cnt.fill_(-7)
+    run.select(flags=run.flags | sp.SP_GRAM_ONLY)
+    torch.cuda.synchronize()
+    assert (run.kept_cnt.cpu().numpy() == -7).all()
+    run.select(flags=run.flags | sp.SP_REUSE_GRAM)
+    torch.cuda.synchronize()
+    _check_errors(run)
+    assert run.kept_lists() == kept
+    # bitwise: records past an episode's end hold int32 -2, a NaN as float
+    assert torch.equal(run.trace.view(torch.int32), tr.view(torch.int32))
+
+
 def test_immediate_stop(gpu_lib):
     """b_stop = +inf: every episode stops at its first step (K = 0) and the
     prefill holds only the prompt rows."""
