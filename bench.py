@@ -231,6 +231,9 @@ def main(argv=None):
     ap.add_argument("--streams", type=int, default=3,
                     help="streams of the pipelined pass: select streams (staggered, at most 3) "
                          "or round-robin streams (rr); 1: no pipelined pass")
+    ap.add_argument("--hw-queues", type=int, default=0,
+                    help="set GPU_MAX_HW_QUEUES (at most 32) for this process before HIP starts, "
+                         "to run more pipelined streams on queues of their own (0: leave it)")
     ap.add_argument("--slots", type=int, default=4,
                     help="buffer slots of the staggered pipelined pass (batches in flight)")
     ap.add_argument("--schedule", choices=["staggered", "staggered-gram", "rr"], default="staggered",
@@ -249,6 +252,11 @@ def main(argv=None):
                     help="only run a plain device copy of this many MiB (5 launches), the "
                          "calibration for the FETCH_SIZE / WRITE_SIZE counters, and exit")
     args = ap.parse_args(argv)
+    if args.hw_queues:
+        if not 1 <= args.hw_queues <= 32:
+            print("--hw-queues must be 1..32", file=sys.stderr)
+            return 2
+        os.environ["GPU_MAX_HW_QUEUES"] = str(args.hw_queues)   # read when HIP starts
     if args.copy_probe_mib:
         return copy_probe(args.copy_probe_mib)
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -399,7 +407,7 @@ def main(argv=None):
     if S > 1:
         from paper_2609_13804_amd.runner import Pipeline
         if args.schedule.startswith("staggered"):
-            pipe = Pipeline(run, max(S, args.slots), min(S, Pipeline.MAX_STREAMS),
+            pipe = Pipeline(run, max(S, args.slots), min(S, Pipeline.max_streams()),
                             split_gram=args.schedule == "staggered-gram")
             runs = pipe.runs
             issue = lambda k: pipe.issue()

@@ -4,6 +4,7 @@ Plumbing only: torch allocates HBM and provides the stream; every stage runs
 in libstepprune's kernels through the binding.
 """
 import copy
+import os
 from dataclasses import dataclass
 from typing import Dict, Optional
 
@@ -227,11 +228,16 @@ class Pipeline:
     stream on a hardware queue of its own under HIP's default of four per
     process."""
 
-    MAX_STREAMS = 3
+    @staticmethod
+    def max_streams() -> int:
+        """Select streams that keep every stream of the pipeline (plus the
+        caller's) on a hardware queue of its own: GPU_MAX_HW_QUEUES - 1 (HIP's
+        default of four queues gives three)."""
+        return max(1, int(os.environ.get("GPU_MAX_HW_QUEUES", "4")) - 1)
 
     def __init__(self, run: DeviceRun, slots: int = 4, streams: int = 3, split_gram: bool = False):
-        if not 1 <= streams <= self.MAX_STREAMS:
-            raise ValueError(f"streams must be 1..{self.MAX_STREAMS}")
+        if not 1 <= streams <= self.max_streams():
+            raise ValueError(f"streams must be 1..{self.max_streams()}")
         if slots < streams:
             raise ValueError("need at least one slot per select stream")
         self.runs = [run] + [run.sibling() for _ in range(slots - 1)]
