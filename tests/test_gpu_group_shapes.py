@@ -4,6 +4,7 @@ element by element against the oracle (tests/parity.py protocol):
   * up to 512 tokens: one lane per token column;
   * 513-576 tokens: wave 0's lanes also own the columns past 512;
   * more than 576 tokens: 16 waves with fewer history registers per lane;
+  * a largest group of 256 or 512 tokens: the Gram products' edge layout;
 
 with caps that keep the history in registers, and caps that push it through
 the LDS rows and the re-read tier.  Each case runs the untraced kernel (the
@@ -27,6 +28,11 @@ CASES = [
     ("second_cols_576", 106, (576, 513, 512, 65), 64, 0.25),
     ("second_cols_deep", 107, (513, 520), 300, -math.inf),
     ("lanes_512", 108, (512, 448, 64, 1), 40, 0.1),
+    # largest group a multiple of 256: the Gram tiles cover the token blocks
+    # only and a separate kernel computes the START / STOP / context entries
+    ("edge_256", 115, (256, 100, 255, 1, 254), 40, 0.1),
+    ("edge_256_deep", 116, (256, 256), 200, -math.inf),
+    ("edge_512", 117, (512, 300), 48, 0.1),
 ]
 
 

@@ -303,3 +303,27 @@ def test_long_episodes_cross_every_history_tier(gpu_lib):
                                  actions, run.trace.cpu().numpy(), w.dtype)
     print(f"long episodes: {rep.steps} steps, {rep.exempt_steps} exempt, "
           f"max logit err {rep.max_logit_err:.2e}")
+
+
+def test_pipeline_slots_agree_with_one_stream(gpu_lib):
+    """runner.Pipeline (projections on one stream, selections and compactions
+    on three streams over four buffer slots, events between them) gives every
+    slot the single-stream run's kept lists and prefill buffer, bit for bit,
+    in both schedules."""
+    from paper_2609_13804_amd.runner import Pipeline
+    for split in (False, True):
+        w, inp, lay, run = _setup("small_packed_bf16", trace=False)
+        run.run()
+        torch.cuda.synchronize()
+        want_kept, want_out = run.kept_lists(), run.out.clone()
+        for r_ in [run]:
+            r_.kept_idx.fill_(-1)
+            r_.out.zero_()
+        pipe = Pipeline(run, slots=4, streams=3, split_gram=split)
+        for _ in range(9):
+            pipe.issue()
+        torch.cuda.synchronize()
+        for r_ in pipe.runs:
+            assert r_.device_errors() == [0, 0, 0]
+            assert r_.kept_lists() == want_kept
+            assert torch.equal(r_.out, want_out)
