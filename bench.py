@@ -262,7 +262,7 @@ def main(argv=None):
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU only: the selection path shards by image with no "
-              "communication, and this build measures the one-GPU share (--gpus 1).",
+              "communication, and bench.py measures the one-GPU share (--gpus 1).",
               file=sys.stderr)
         return 2
 
@@ -373,7 +373,7 @@ def main(argv=None):
     sel_amount = work["select_recurrence"][1]
     # The selector against a roofline that assumes a per-step scan of the
     # unselected keys from LDS plus one HBM read of the keys and the history
-    # rows (the traffic model this build's Gram rewrite replaces): the time
+    # rows (the traffic model that the Gram rewrite used here replaces): the time
     # the scan's bytes would take at the LDS and HBM peaks, over the measured
     # select stage.
     eb_keys = eb

@@ -63,7 +63,7 @@ extern "C" {
 typedef enum {
   SP_OK = 0,
   SP_EINVAL = 1,        /* a host-side argument is invalid (null, size, alignment) */
-  SP_EUNSUPPORTED = 2,  /* valid but not supported by this build (dtype, g > 1, sizes) */
+  SP_EUNSUPPORTED = 2,  /* valid but not supported by this library (dtype, g > 5, sizes) */
   SP_EWORKSPACE = 3,    /* ws_bytes smaller than stepprune_workspace_bytes() */
   SP_EHIP = 4,          /* a HIP launch or runtime call failed */
   SP_EDEVICE = 5        /* the device error word is set (read_device_error) */
