@@ -661,7 +661,7 @@ __global__ __launch_bounds__(256) void gram_edge_kernel(GramArgs a) {
 // token blocks only, [Q] x [K] into A's rows 0..n-1 and [V] x [K] into B's
 // rows 0..n-1 (tq x tq tiles each), and gram_edge_kernel computes the rows
 // and columns of START, STOP and the context split.
-constexpr int kGramWaves = 4;
+constexpr int kGramWaves = 8;
 
 __global__ __launch_bounds__(64 * kGramWaves) void gram_gemm_bf16_kernel(GramArgs a, int per_group,
                                                                  int xcd_grouped, int edge) {
