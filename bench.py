@@ -142,6 +142,74 @@ def _oracle_sample(w, b_stop, budget_s, threads):
                       f"float64, {elapsed:.1f} s"}
 
 
+def host_info():
+    """The host the CPU baseline ran on: CPU model, cores visible to this
+    process, and the BLAS library NumPy's products use with its thread count."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    info = {"cpu_model": model, "cpu_count": os.cpu_count(),
+            "affinity": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None}
+    try:
+        from threadpoolctl import threadpool_info
+        info["blas"] = [{"api": i.get("internal_api"), "threads": i.get("num_threads")}
+                        for i in threadpool_info() if i.get("user_api") == "blas"]
+    except Exception:
+        info["blas"] = None
+    return info
+
+
+def measured_peaks():
+    """Rates this GPU reaches on plain library work, the second denominator for
+    the stage fractions: HBM from a 1 GiB device-to-device copy (bytes read plus
+    bytes written), bf16 matrix throughput from the best of torch's bf16
+    matmuls (hipBLASLt) over three shapes.  Timed with events on torch's
+    current stream, where they run."""
+    import torch
+    res = {}
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").random_(0, 255)
+    dst = torch.empty_like(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(3):
+        dst.copy_(src)
+    e0.record()
+    for _ in range(10):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    res["hbm_copy_GBs"] = round(2 * n * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
+    del src, dst
+    # a square shape, a tall one, and the 16-image batch's projection (without
+    # its START / STOP rows); X [M, K] times W^T with W stored [N, K], the
+    # layout the library's projection takes (a two-dimensional product, no batch)
+    rates = {}
+    for (mm, kk, nn) in [(8192, 8192, 8192), (16384, 4096, 4096), (9216, 4096, 3072)]:
+        a = torch.randn(mm, kk, device="cuda").to(torch.bfloat16)
+        b = torch.randn(nn, kk, device="cuda").to(torch.bfloat16)
+        for _ in range(3):
+            c = a @ b.t()
+        e0.record()
+        for _ in range(10):
+            c = a @ b.t()
+        e1.record()
+        torch.cuda.synchronize()
+        rates[f"{mm}x{kk}x{nn}"] = round(2.0 * mm * kk * nn * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e12, 1)
+        del a, b, c
+    torch.cuda.empty_cache()
+    res["bf16_matmul_TFLOPs"] = max(rates.values())
+    res["bf16_matmul_by_shape"] = rates
+    res["how"] = ("1 GiB device copy (read + write bytes); the best torch bf16 matmul rate "
+                  "(M x K x N) of the shapes listed; 10 launches each after 3 warm-up")
+    return res
+
+
 def copy_probe(mib):
     """A plain device-to-device copy of a known size: under rocprofv3 --pmc its
     FETCH_SIZE and WRITE_SIZE readings calibrate the same counters taken on the
@@ -450,6 +518,21 @@ def main(argv=None):
                 raise RuntimeError("streams disagree on the same batch")
         elapsed = t1 - t0
     value = K * s.B / elapsed
+
+    # Second denominators: what plain library work reaches on this GPU.
+    peaks = measured_peaks()
+    mpeak = {"mfma": peaks["bf16_matmul_TFLOPs"] if w.dtype == "bf16" else None,
+             "hbm": peaks["hbm_copy_GBs"]}
+    if mpeak["mfma"]:
+        stage_roofline["project"]["frac_measured_peak"] = frac(
+            proj_flop + text_flop, mpeak["mfma"], stages["project"])
+        stage_roofline["select"]["frac_gram_measured_peak"] = frac(
+            gram_flop, mpeak["mfma"], kernels["gram_gemm"])
+    stage_roofline["compact"]["frac_measured_peak"] = frac(
+        work["compact_gather"][1], mpeak["hbm"], stages["compact"])
+    if mpeak.get(roofline["bound"]):
+        roofline["measured_peak"] = mpeak[roofline["bound"]]
+        roofline["frac_measured_peak"] = round(roofline["achieved"] / mpeak[roofline["bound"]], 4)
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -476,6 +559,7 @@ def main(argv=None):
         "stages_us": {k: round(v, 2) for k, v in stages.items()},
         "stages_us_pct": {k: {q: round(x, 2) for q, x in v.items()} for k, v in stage_pct.items()},
         "stage_roofline": stage_roofline,
+        "measured_peaks": peaks,
         "kernels_us": {k: round(v, 2) for k, v in kernels.items()},
         "selection_steps_per_s": round(sum(steps_g) / (stages["select"] * 1e-6), 1),
         "roofline": roofline,
@@ -493,6 +577,7 @@ def main(argv=None):
         one = cpu_baseline(w, lay, b_stop, args.cpu_budget * 0.5, single_thread=True)
         out["cpu_baseline"]["single_core"] = {"value": one["value"], "unit": one["unit"],
                                               "sample": one["sample"]}
+        out["cpu_baseline"]["host"] = host_info()
     print(json.dumps(out), flush=True)
     return 0
 
