@@ -150,3 +150,46 @@ def test_compact_validation(sp):
 def test_read_device_error_rejects_null(sp):
     code = ctypes.c_int32(0)
     assert sp.library().stepprune_read_device_error(None, None, ctypes.byref(code)) == sp.SP_EINVAL
+
+
+C_PROGRAM = r"""
+#include <stdio.h>
+#include "stepprune.h"
+int main(void) {
+  sp_dims d = {4096, 4096, 1024, SP_BF16};
+  for (int s = SP_OK; s <= SP_EDEVICE; ++s) printf("%s\n", stepprune_status_string((sp_status)s));
+  printf("%zu\n", stepprune_workspace_bytes(1, &d, 9216, 1024, 16, 16, 576, 192));
+  /* host validation only: a null dims pointer and null buffers never reach the device */
+  printf("%d\n", (int)stepprune_project(NULL, NULL, 0, NULL, NULL, NULL, NULL, NULL, 1, 0, NULL,
+                                        1.0f, 1e-5f, NULL, NULL, NULL, 0, NULL, 0));
+  printf("%d\n", (int)stepprune_compact(&d, NULL, NULL, NULL, NULL, NULL, NULL, NULL, 1,
+                                        SP_LAYOUT_PADDED, 640, 0, NULL, NULL, NULL, 0, NULL, 0));
+  return 0;
+}
+"""
+
+
+def test_header_is_plain_c(sp, tmp_path):
+    """A C99 program compiled by gcc against the header alone links the library
+    and gets the same answers the Python binding gets."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    rocm_inc = "/opt/rocm/include"
+    if gcc is None or not os.path.isdir(rocm_inc):
+        pytest.skip("gcc or the ROCm headers are not available")
+    src = tmp_path / "abi.c"
+    src.write_text(C_PROGRAM)
+    lib_dir = os.path.dirname(sp.LIB_PATH)
+    exe = tmp_path / "abi"
+    subprocess.run([gcc, "-std=c99", "-Wall", "-Werror=implicit-function-declaration",
+                    "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"), "-I", rocm_inc,
+                    str(src), "-o", str(exe), "-L", lib_dir, "-lstepprune",
+                    f"-Wl,-rpath,{lib_dir}"], check=True, capture_output=True, timeout=120)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True,
+                         timeout=60).stdout.split("\n")
+    assert out[:6] == [sp.status_string(s) for s in range(6)]
+    assert int(out[6]) == sp.stepprune_workspace_bytes(1, sp.dims(4096, 4096, 1024, sp.SP_BF16),
+                                                       9216, 1024, 16, 16, 576, 192)
+    assert int(out[7]) == sp.SP_EINVAL
+    assert int(out[8]) == sp.SP_EINVAL
