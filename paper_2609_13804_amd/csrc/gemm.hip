@@ -2,21 +2,22 @@
 //
 //   C[m, n] = sum_k A[m, k] * B[n, k]      (both operands K-contiguous)
 //
-// bfloat16 operands use v_mfma_f32_32x32x16_bf16, float32 operands
-// v_mfma_f32_32x32x2_f32; accumulation is float32 and the result is stored
-// once (bfloat16 rounded to nearest-even, or float32).  A workgroup of four
-// waves owns a BM x BN tile; each wave owns a (BM/2) x (BN/2) quadrant made
-// of 32 x 32 MFMA tiles.  K is walked in BK-wide stages through two LDS
-// buffers: the next stage is fetched into registers while the current one
-// feeds the matrix cores, then written to the other buffer, so one barrier
-// per stage suffices.
+// Accumulation is float32 and the result is stored once (bfloat16 rounded to
+// nearest-even, or float32).  Two cores:
+//  * bfloat16, gemm_bf16_256: 256 x 256 tiles of eight waves, each wave owning
+//    128 x 64 as 32 x 32 tiles of v_mfma_f32_32x32x16_bf16; K in 32-wide
+//    stages through a four-deep LDS ring filled straight from global memory.
+//  * float32, gemm_block: BM x BN tiles of four waves, each owning a
+//    (BM/2) x (BN/2) quadrant of 32 x 32 tiles of v_mfma_f32_32x32x2_f32; K in
+//    BK-wide stages through two LDS buffers, the next stage fetched into
+//    registers while the current one feeds the matrix cores.
 //
 // Three users:
 //  * the projection of Algorithm 1 step 1: A = [X; s_start; s_stop], B = W_kqv;
 //  * the text projection W_text E_text^T (float32 output for the LayerNorm);
 //  * per-group Gram products of the projected rows used by the selection
-//    recurrence (select.hip): rows [Q_g; q_start; V_g; v_start] against
-//    columns [K_g; k_stop; k_start].
+//    recurrence (select.hip): rows [Q_g; q_start; V_g; v_start; context split]
+//    against columns [K_g; k_stop; k_start].
 #include "sp_internal.h"
 
 namespace sp {
@@ -41,11 +42,12 @@ __device__ inline float store_cvt<float>(float v) { return v; }
 template <>
 __device__ inline uint16_t store_cvt<uint16_t>(float v) { return f32_to_bf16_rne(v); }
 
+// Geometry of the float32 core's tiles.
 template <typename T, int BM, int BN, int BK>
 struct Tile {
+  static_assert(sizeof(T) == 4, "the register-staged core is float32 only");
   static constexpr int VEC = 16 / (int)sizeof(T);      // elements per 16-byte chunk
-  static constexpr bool BF16 = sizeof(T) == 2;
-  static constexpr int KM = BF16 ? 16 : 2;              // K of one MFMA
+  static constexpr int KM = 2;                          // K of one MFMA
   static constexpr int LDK = BK + VEC;                  // padded LDS row, elements
   static constexpr int CPR = BK / VEC;                  // chunks per tile row
   static constexpr int CH_A = BM * CPR / kThreads;      // chunks per thread per stage
@@ -130,33 +132,17 @@ __device__ __forceinline__ void gemm_block(const ARows& ar, const BRows& br, int
     const T* Bb = Bs + buf * BN * G::LDK;
 #pragma unroll
     for (int ks = 0; ks < BK; ks += G::KM) {
-      if constexpr (G::BF16) {
-        bf16x8_t a[G::TM], b[G::TN];
-        const int koff = ks + (lane >> 5) * 8;
+      float a[G::TM], b[G::TN];
+      const int koff = ks + (lane >> 5);
 #pragma unroll
-        for (int i = 0; i < G::TM; ++i)
-          a[i] = *reinterpret_cast<const bf16x8_t*>(Ab + (arow + i * 32) * G::LDK + koff);
+      for (int i = 0; i < G::TM; ++i) a[i] = Ab[(arow + i * 32) * G::LDK + koff];
+#pragma unroll
+      for (int j = 0; j < G::TN; ++j) b[j] = Bb[(brow + j * 32) * G::LDK + koff];
+#pragma unroll
+      for (int i = 0; i < G::TM; ++i)
 #pragma unroll
         for (int j = 0; j < G::TN; ++j)
-          b[j] = *reinterpret_cast<const bf16x8_t*>(Bb + (brow + j * 32) * G::LDK + koff);
-#pragma unroll
-        for (int i = 0; i < G::TM; ++i)
-#pragma unroll
-          for (int j = 0; j < G::TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-      } else {
-        float a[G::TM], b[G::TN];
-        const int koff = ks + (lane >> 5);
-#pragma unroll
-        for (int i = 0; i < G::TM; ++i) a[i] = Ab[(arow + i * 32) * G::LDK + koff];
-#pragma unroll
-        for (int j = 0; j < G::TN; ++j) b[j] = Bb[(brow + j * 32) * G::LDK + koff];
-#pragma unroll
-        for (int i = 0; i < G::TM; ++i)
-#pragma unroll
-          for (int j = 0; j < G::TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
-      }
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
     }
     if (kt + 1 < KT) lstore(buf ^ 1);
     __syncthreads();
