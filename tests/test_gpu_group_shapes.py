@@ -2,7 +2,8 @@
 element by element against the oracle (tests/parity.py protocol):
 
   * up to 512 tokens: one lane per token column;
-  * 513-576 tokens: wave 0's lanes also own the columns past 512;
+  * 513-576 tokens: waves 0-3 also own the columns past 512, a quarter of
+    each column's history per lane;
   * more than 576 tokens: 16 waves with fewer history registers per lane;
   * a largest group of 256 or 512 tokens: the Gram products' edge layout;
 

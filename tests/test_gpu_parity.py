@@ -206,6 +206,56 @@ def test_duplicate_rows_identical_logits(gpu_lib):
                            run.trace_actions(), run.trace.cpu().numpy(), w.dtype)
 
 
+@pytest.mark.parametrize("name", ["mid_bf16", "mid_g5_bf16"])
+def test_permutation_equivariance_is_bit_exact(gpu_lib, name):
+    """Permuting the tokens inside each group permutes the decisions and leaves
+    every traced logit bit-identical (pin P8 on the GPU): a token's projected
+    row and its Gram entries are accumulated in the same order wherever the
+    token sits, and the history sums run in history order (with g = 5 a
+    round's tokens enter it in descending-logit order).  Columns 512 and up of
+    a 576-token group are summed in quarters by other lanes, so tokens are
+    permuted within [0, 512) and within [512, n) separately."""
+    from paper_2609_13804_amd.runner import DeviceRun
+    w = W.WORKLOADS[name]
+    inp = W.make_inputs(w)
+    lay = W.make_layout(w)
+    steps = int(lay.grp_cap.max()) + 1
+    rng = np.random.default_rng(8808)
+    P = np.arange(int(lay.img_off[-1]))
+    local = []
+    for g in range(lay.groups):
+        g0, g1 = int(lay.grp_off[g]), int(lay.grp_off[g + 1])
+        perm = np.arange(g1 - g0)
+        for lo, hi in ((0, min(512, g1 - g0)), (512, g1 - g0)):
+            if hi > lo:
+                perm[lo:hi] = lo + rng.permutation(hi - lo)
+        P[g0:g1] = g0 + perm
+        local.append(perm)              # new position p holds old token perm[p]
+    res = []
+    for X in (inp["X"], inp["X"][P]):
+        run = DeviceRun(w, dict(inp, X=X), lay, W.stop_bias(w), trace_steps=steps)
+        run.run()
+        torch.cuda.synchronize()
+        _check_errors(run)
+        res.append((run.trace_actions(), run.trace.cpu().numpy().copy()))
+        del run
+    (a0, t0), (a1, t1) = res
+    k = w.g                             # trace slots holding taken tokens
+    for g in range(lay.groups):
+        new_pos = np.argsort(local[g])  # old token -> new position
+        n = len(a0[g])
+        assert n > 1
+        # no decision rested on an exact tie: the (smallest) taken logit is
+        # strictly above the best candidate left out
+        assert np.all(t0[g, :n, k] != t0[g, :n, k + 1]), g
+        if k == 1:
+            want = [int(new_pos[x]) if x >= 0 else -1 for x in a0[g]]
+        else:
+            want = [[int(new_pos[x]) if x >= 0 else -1 for x in r] for r in a0[g]]
+        assert a1[g] == want, g
+        assert np.array_equal(t1[g, :n, k:].view(np.uint32), t0[g, :n, k:].view(np.uint32)), g
+
+
 def test_zero_caps_and_episode_independence(gpu_lib):
     """Cap 0 gives an empty episode without any step; a sub-batch in another
     order gives the same per-image results (episodes are independent)."""
