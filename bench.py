@@ -142,6 +142,51 @@ def _oracle_sample(w, b_stop, budget_s, threads):
                       f"float64, {elapsed:.1f} s"}
 
 
+def steady_pass(w, R, b_stop, hip, stream, t_scan_roof, ref_kept, steps=10, warmup=2):
+    """Secondary, labelled steady-state figure for the selection stage: R copies
+    of the batch in one call of each stage, so the recurrence runs R times as
+    many episodes at once (up to one per compute unit) and the per-batch select
+    time approaches its throughput rather than the longest episode's latency."""
+    import numpy as np
+    from paper_2609_13804_amd import workloads as W
+    from paper_2609_13804_amd.runner import DeviceRun
+    inp = W.make_inputs(w)
+    inp["X"] = np.tile(inp["X"], (R, 1))
+    inp["E_text"] = np.tile(inp["E_text"], (R, 1))
+    lay = W.make_layout(w, list(range(w.batch)) * R)
+    run = DeviceRun(w, inp, lay, b_stop)
+    run.flags = 0
+    del inp
+    for _ in range(warmup):
+        run.run(stream)
+    names = ["sel0", "gram0", "gram1", "rec0", "rec1", "sel1"]
+    evs = [{n: hip.create() for n in names} for _ in range(steps)]
+    for e in evs:
+        run.project(stream)
+        hip.record(e["sel0"], stream)
+        run.select(stream, events=[e["gram0"], e["gram1"], e["rec0"], e["rec1"]])
+        hip.record(e["sel1"], stream)
+        run.compact(stream)
+    import torch
+    torch.cuda.synchronize()
+    if any(run.device_errors()):
+        raise RuntimeError(f"device error words {run.device_errors()}")
+    kept = run.kept_lists()
+    if any(kept[r * w.batch:(r + 1) * w.batch] != ref_kept for r in range(R)):
+        raise RuntimeError("a copy of the batch selected differently from the batch alone")
+    mean = lambda a, b: float(np.mean([1e3 * hip.ms(e[a], e[b]) for e in evs]))
+    sel, gram, rec = mean("sel0", "sel1"), mean("gram0", "gram1"), mean("rec0", "rec1")
+    for e in evs:
+        for ev in e.values():
+            hip.destroy(ev)
+    return {"copies": R, "images": R * w.batch, "episodes": int(lay.grp_off.size - 1),
+            "select_us": round(sel, 2), "gram_us": round(gram, 2), "recurrence_us": round(rec, 2),
+            "select_us_per_batch": round(sel / R, 2),
+            "frac_keyscan_roofline": round(R * t_scan_roof / (sel * 1e-6), 4),
+            "note": "secondary figure: R copies of the batch per call of each stage; "
+                    "not the headline value"}
+
+
 def host_info():
     """The host the CPU baseline ran on: CPU model, cores visible to this
     process, and the BLAS library NumPy's products use with its thread count."""
@@ -313,6 +358,9 @@ def main(argv=None):
     ap.add_argument("--trajectory", type=float, nargs=2, metavar=("TAU", "BETA"), default=None,
                     help="also time the selection with the trajectory sums of Eqs. 5-7 over the "
                          "full rollout (stepprune_select_trajectory) against the plain selection")
+    ap.add_argument("--steady", type=int, default=0, metavar="R",
+                    help="also time the selection stage on R copies of the batch in one call "
+                         "(R x the episodes at once): a secondary steady-state figure")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle work for the CPU baseline sample")
@@ -572,6 +620,9 @@ def main(argv=None):
     }
     if args.trajectory is not None:
         out["trajectory"] = trajectory_pass(run, args.trajectory, K, hip)
+    if args.steady > 0:
+        out["select_steady"] = steady_pass(w, args.steady, b_stop, hip, stream, t_scan_roof,
+                                           run.kept_lists())
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, lay, b_stop, args.cpu_budget)
         one = cpu_baseline(w, lay, b_stop, args.cpu_budget * 0.5, single_thread=True)
