@@ -333,6 +333,53 @@ def test_device_error_on_oversized_group(gpu_lib):
     assert sp.stepprune_read_device_error(run.ws[1]) == 0     # read clears it
 
 
+@pytest.mark.parametrize("case", ["negative_cap", "cap_above_max", "group_outside_image",
+                                  "text_offsets_decrease", "packed_output_too_small"])
+def test_device_errors_from_bad_data(gpu_lib, case):
+    """Data that only the device sees (offsets, caps, counts) and that is
+    inconsistent is caught by the kernels' own checks: the stage records the
+    documented SP_DEV_* code in its workspace, and reading it clears it.  Each
+    case corrupts one device array after a valid set-up; every kernel still
+    reads and writes inside its buffers."""
+    from paper_2609_13804_amd import binding as sp
+    name = "small_packed_bf16" if case == "packed_output_too_small" else "tiny_bf16"
+    w, inp, lay, run = _setup(name, trace=False)
+    if case == "text_offsets_decrease":
+        run.text_off[2] = int(lay.text_off[1]) - 1
+        run.project()
+        torch.cuda.synchronize()
+        assert sp.stepprune_read_device_error(run.ws[0]) == sp.SP_DEV_BAD_OFFSETS
+        assert not run.ctx[1].any()          # the image with no valid text gets c = 0
+        assert sp.stepprune_read_device_error(run.ws[0]) == 0
+        return
+    run.project()
+    if case == "negative_cap":
+        run.grp_cap[1] = -1
+        want, stage = sp.SP_DEV_BAD_CAP, 1
+    elif case == "cap_above_max":
+        run.grp_cap[0] = 10 ** 6             # min(cap, n) exceeds the stated max_cap
+        want, stage = sp.SP_DEV_BAD_CAP, 1
+    elif case == "group_outside_image":
+        run.grp_img[0] = 1                   # group 0's rows lie in image 0
+        want, stage = sp.SP_DEV_BAD_OFFSETS, 1
+    else:
+        run.select()
+        torch.cuda.synchronize()
+        _check_errors(run)
+        run.compact()
+        torch.cuda.synchronize()
+        need = int(run.seq_info[-1])         # rows the packed buffer needs
+        sp.stepprune_compact(run.dims, run.X, run.img_off, run.E, run.text_off, run.kept_idx,
+                             run.kept_off, run.kept_cnt, run.sizes.B, run.layout_code, 0,
+                             need - 1, run.out, run.seq_info, run.ws[2], run.ws_bytes[2])
+        want, stage = sp.SP_DEV_OUTPUT_OVERFLOW, 2
+    if stage == 1:
+        run.select()
+    torch.cuda.synchronize()
+    assert sp.stepprune_read_device_error(run.ws[stage]) == want
+    assert sp.stepprune_read_device_error(run.ws[stage]) == 0
+
+
 def test_long_episodes_cross_every_history_tier(gpu_lib):
     """Episodes far longer than the register-resident history: caps of 400 on
     576-token groups with STOP disabled, so the history passes the register
