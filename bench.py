@@ -9,17 +9,25 @@ the LLaVA-1.5-shaped one: 16 images x 576 tokens x 4096, bf16, selector
 hidden width 1024, cap 192, STOP bias set so that the mean retained count is
 about 64, compaction into 576 + 64 prefill rows.
 
-Two timed passes over K steps each: one stream running the batches one after
-another (per-stage and per-kernel times from HIP events the library records on
-that stream; reported as "single_stream"), then S streams taking consecutive
-batches in turn, each with its own outputs and workspaces, so that one batch's
-projection runs beside another batch's recurrence ("value", the whole job's
-throughput).  Prints one JSON line.  The roofline object covers the kernel with
-the largest average duration in the single-stream pass; the CPU baseline is
-the float64 oracle timed on this host's cores over a bounded sample of the
-same batch.
+Two timed passes over K steps each, after W untimed warm-up steps:
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--streams 3] [--workload llava15_bf16]
+  * single stream: the batches one after another on one stream, with per-stage
+    and per-kernel times from HIP events the library records on that stream
+    ("single_stream", "stages_us", "kernels_us", "stage_roofline");
+  * pipelined (the reported "value", whole-job throughput): projections on one
+    stream in batch order and each batch's select + compact on one of S select
+    streams over a ring of buffer slots (runner.Pipeline), so that one batch's
+    projection and Gram products run beside earlier batches' recurrences; at
+    least 64 untimed batches fill and warm the pipeline first.
+
+Prints one JSON line.  "roofline" covers the kernel with the largest share of
+the GPU (kernel time x fraction of the compute units it occupies), with its HBM
+traffic from the committed counter summary; "measured_peaks" adds rates this
+GPU reaches on library work; "cpu_baseline" is the float64 oracle timed on this
+host's cores over a bounded sample of the same batch.
+
+    python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--streams 3] [--slots 4]
+                    [--workload llava15_bf16] [--trajectory TAU BETA] [--steady R]
 """
 import argparse
 import ctypes
