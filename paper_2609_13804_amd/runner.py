@@ -1,7 +1,8 @@
-"""Device buffers for one batch and the three library calls in order.
+"""Device buffers for one batch and the three library calls in order
+(DeviceRun), and a stream of batches overlapped across streams (Pipeline).
 
-Plumbing only: torch allocates HBM and provides the stream; every stage runs
-in libstepprune's kernels through the binding.
+Plumbing only: torch allocates HBM and provides the streams and events; every
+stage runs in libstepprune's kernels through the binding.
 """
 import copy
 import os
