@@ -15,6 +15,7 @@ Modules
   selection    Algorithm 1 steps 2-4: the pointer recurrence with STOP (Eq. 4)
   trajectory   the trajectory sums of the training surrogate (Eqs. 5-7)
   compaction   Algorithm 1 step 5: gather of kept tokens ahead of the prompt
+  denoise      the training pathway's noise gate (Eq. 9) and masked denoiser
   calibration  the STOP bias that gives a target mean retained count
 
 Every function states the passage it follows.  Readings of points the paper
@@ -27,10 +28,12 @@ from .selection import (StepRecord, EpisodeResult, SelectResult, run_episode,
 from .trajectory import TrajectoryResult, step_distribution, aggregate, run_trajectory
 from .compaction import compact
 from .calibration import stop_thresholds, choose_stop_bias
+from .denoise import DenoiserParams, vp_gate, denoise, gate_denoise
 
 __all__ = [
     "round_bf16", "round_f32", "round_to", "project", "text_context", "layer_norm",
     "StepRecord", "EpisodeResult", "SelectResult", "run_episode", "select", "STOP",
     "compact", "stop_thresholds", "choose_stop_bias",
     "TrajectoryResult", "step_distribution", "aggregate", "run_trajectory",
+    "DenoiserParams", "vp_gate", "denoise", "gate_denoise",
 ]
