@@ -269,8 +269,58 @@ sp_status stepprune_compact(const sp_dims* dims,
                             void* ws, size_t ws_bytes,
                             const hipEvent_t* events, hipStream_t stream);
 
-/* Workspace bytes for stage `which` (0 project, 1 select, 2 compact) at the
-   given sizes (host).  Returns 0 for invalid arguments. */
+/* ---------------------------------------------------------------------------
+ * Training pathway: the variance-preserving noise gate and the locally masked
+ * denoiser (Section "Trajectory-Aware Differentiable Optimization": Eq. 9 and
+ * the denoiser paragraph).  Per visual token i (row of X):
+ *
+ *   x~_i = sqrt(a_i) x_i + sqrt(1 - a_i) eps_i
+ *   h_i  = x~_i + W_o (W_v LN1(x~_i) + b_v) + b_o
+ *   y_i  = h_i + W_2 GELU(W_1 LN2(h_i) + b_1) + b_2
+ *
+ * The denoiser is one pre-norm transformer block whose self-attention is
+ * restricted to the diagonal: each token attends only to itself, so its
+ * attention output is the value projection and no information moves between
+ * tokens.  LN is LayerNorm over d with scale and shift (eps 1e-6, biased
+ * variance); GELU is the exact x Phi(x); the hidden width is 4d.  The gate's
+ * weights a_i come from Eq. 8's differentiable top-k in the paper and are an
+ * input here; eps holds the caller's N(0, 1) draws.
+ *
+ * bfloat16 only (SP_EUNSUPPORTED otherwise).  Weights use the [out, in]
+ * layout; vectors are float32.  The residual stream is float32; every product
+ * operand and result is rounded once to bfloat16.  d <= 4096.
+ */
+typedef struct {
+  const float* ln1_g;  /* [d] */
+  const float* ln1_b;  /* [d] */
+  const void* W_v;     /* [d, d] bfloat16 */
+  const float* b_v;    /* [d] */
+  const void* W_o;     /* [d, d] bfloat16 */
+  const float* b_o;    /* [d] */
+  const float* ln2_g;  /* [d] */
+  const float* ln2_b;  /* [d] */
+  const void* W_1;     /* [4d, d] bfloat16 */
+  const float* b_1;    /* [4d] */
+  const void* W_2;     /* [d, 4d] bfloat16 */
+  const float* b_2;    /* [d] */
+} sp_denoiser;
+
+/*  X      [T, d] bfloat16 visual rows;  alpha [T] float32 in [0, 1] (values
+ *         outside give NaN rows);  eps [T, d] bfloat16
+ *  p      (host) the block's parameters, all device pointers, none NULL
+ *  out    [T, d] bfloat16 (may not alias X or eps)
+ *  ws     workspace of stepprune_workspace_bytes(3, dims, T, ...): float32
+ *         [T, d] and bfloat16 [T, d] x 2 and [T, 4d] intermediates
+ *  events [0] before, [1] after the whole block (or NULL)
+ */
+sp_status stepprune_gate_denoise(const sp_dims* dims, const void* X, int64_t T,
+                                 const float* alpha, const void* eps, const sp_denoiser* p,
+                                 void* out, void* ws, size_t ws_bytes,
+                                 const hipEvent_t* events, hipStream_t stream);
+
+/* Workspace bytes for stage `which` (0 project, 1 select, 2 compact, 3 gate
+   and denoiser; for 3, T_vis is the token count T) at the given sizes (host).
+   Returns 0 for invalid arguments. */
 size_t stepprune_workspace_bytes(int32_t which, const sp_dims* dims, int64_t T_vis,
                                  int64_t T_txt, int32_t B, int32_t G,
                                  int32_t max_group, int32_t max_cap);

@@ -21,7 +21,9 @@ SP_DEV_OK, SP_DEV_BAD_OFFSETS, SP_DEV_GROUP_TOO_LARGE, SP_DEV_BAD_CAP, SP_DEV_OU
 STAGE_PROJECT, STAGE_SELECT, STAGE_COMPACT = 0, 1, 2
 
 EXPORTS = ["stepprune_project", "stepprune_select", "stepprune_select_trajectory", "stepprune_compact",
-           "stepprune_workspace_bytes", "stepprune_read_device_error", "stepprune_status_string"]
+           "stepprune_gate_denoise", "stepprune_workspace_bytes", "stepprune_read_device_error",
+           "stepprune_status_string"]
+STAGE_GATE = 3
 
 
 class StepPruneError(RuntimeError):
@@ -39,6 +41,11 @@ class sp_trajectory(ctypes.Structure):
     _fields_ = [("tau", ctypes.c_float), ("beta", ctypes.c_float), ("s", ctypes.c_void_p),
                 ("kbar", ctypes.c_void_p), ("pstop", ctypes.c_void_p),
                 ("pstop_steps", ctypes.c_int32)]
+
+
+class sp_denoiser(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("ln1_g", "ln1_b", "W_v", "b_v", "W_o", "b_o",
+                                               "ln2_g", "ln2_b", "W_1", "b_1", "W_2", "b_2")]
 
 
 if not os.path.exists(LIB_PATH):
@@ -65,6 +72,9 @@ _lib.stepprune_select_trajectory.argtypes = [_DIMS, _P, _P, _I64, _P, _I32, _P, 
 _lib.stepprune_compact.restype = _I32
 _lib.stepprune_compact.argtypes = [_DIMS, _P, _P, _P, _P, _P, _P, _P, _I32, _I32, _I32, _I64, _P, _P,
                                    _P, _SZ, _P, _P]
+_lib.stepprune_gate_denoise.restype = _I32
+_lib.stepprune_gate_denoise.argtypes = [_DIMS, _P, _I64, _P, _P, ctypes.POINTER(sp_denoiser), _P,
+                                        _P, _SZ, _P, _P]
 _lib.stepprune_workspace_bytes.restype = _SZ
 _lib.stepprune_workspace_bytes.argtypes = [_I32, _DIMS, _I64, _I64, _I32, _I32, _I32, _I32]
 _lib.stepprune_read_device_error.restype = _I32
@@ -167,6 +177,19 @@ def stepprune_compact(dm, X, img_off, E_text, text_off, kept_idx, kept_off, kept
                                 layout, rows_per_image, out_rows, _ptr(out), _ptr(seq_info),
                                 _ptr(ws), ws_bytes, _events(events), _stream(stream))
     return _check("stepprune_compact", st, raise_on_error)
+
+
+def denoiser(**tensors) -> sp_denoiser:
+    """The block's parameters (device tensors, by the C field names)."""
+    return sp_denoiser(**{k: _ptr(v) for k, v in tensors.items()})
+
+
+def stepprune_gate_denoise(dm, X, T, alpha, eps, params, out, ws, ws_bytes, stream=None,
+                           raise_on_error=True, events=None):
+    st = _lib.stepprune_gate_denoise(ctypes.byref(dm), _ptr(X), T, _ptr(alpha), _ptr(eps),
+                                     ctypes.byref(params), _ptr(out), _ptr(ws), ws_bytes,
+                                     _events(events), _stream(stream))
+    return _check("stepprune_gate_denoise", st, raise_on_error)
 
 
 def stepprune_read_device_error(ws, stream=None) -> int:

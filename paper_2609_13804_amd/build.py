@@ -16,7 +16,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libstepprune.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["api.hip", "gemm.hip", "select.hip", "text.hip", "compact.hip"]
+SOURCES = ["api.hip", "gemm.hip", "select.hip", "text.hip", "compact.hip", "denoise.hip"]
 # The selection recurrence keeps each column's history in vector registers; let
 # alloca promotion use the whole VGPR budget instead of a quarter of it.
 EXTRA_FLAGS = {"select.hip": ["-mllvm", "-amdgpu-promote-alloca-to-vector-vgpr-ratio=1"]}

@@ -55,6 +55,22 @@ size_t project_ws_bytes(const sp_dims* d, int64_t T_txt) {
 
 sp_status hip_status(hipError_t e) { return e == hipSuccess ? SP_OK : SP_EHIP; }
 
+// Header, then the gate and denoiser's intermediates: x~ / h float32 [T, d],
+// two bfloat16 [T, d] buffers and the bfloat16 [T, 4d] hidden activations.
+struct GateWs {
+  size_t xt, p, q, hid, total;
+};
+GateWs gate_ws_layout(const sp_dims* d, int64_t T) {
+  GateWs w;
+  const size_t td = (size_t)T * d->d;
+  w.xt = kWsHeaderBytes;
+  w.p = align_up(w.xt + td * 4, 256);
+  w.q = align_up(w.p + td * 2, 256);
+  w.hid = align_up(w.q + td * 2, 256);
+  w.total = align_up(w.hid + td * 4 * 2, 256);
+  return w;
+}
+
 }  // namespace
 
 extern "C" {
@@ -80,6 +96,9 @@ size_t stepprune_workspace_bytes(int32_t which, const sp_dims* dims, int64_t T_v
       if (max_group < 0 || max_group > kMaxGroup || max_cap < 0) return 0;
       return select_ws_layout(dims, B, G, max_group, max_cap).total;
     case 2: return kWsHeaderBytes;
+    case 3:
+      if (dims->dtype != SP_BF16 || dims->d > 4096) return 0;
+      return gate_ws_layout(dims, T_vis).total;
   }
   return 0;
 }
@@ -280,6 +299,54 @@ sp_status stepprune_read_device_error(void* ws, hipStream_t stream, int32_t* cod
     return SP_EDEVICE;
   }
   return SP_OK;
+}
+
+sp_status stepprune_gate_denoise(const sp_dims* dims, const void* X, int64_t T,
+                                 const float* alpha, const void* eps, const sp_denoiser* p,
+                                 void* out, void* ws, size_t ws_bytes,
+                                 const hipEvent_t* events, hipStream_t stream) {
+  sp_status st = check_dims(dims);
+  if (st != SP_OK) return st;
+  if (dims->dtype != SP_BF16 || dims->d > 4096) return SP_EUNSUPPORTED;
+  if (T < 0 || !p || !out || !ws) return SP_EINVAL;
+  if (T > 0 && (!X || !alpha || !eps)) return SP_EINVAL;
+  if (!p->ln1_g || !p->ln1_b || !p->W_v || !p->b_v || !p->W_o || !p->b_o || !p->ln2_g ||
+      !p->ln2_b || !p->W_1 || !p->b_1 || !p->W_2 || !p->b_2)
+    return SP_EINVAL;
+  if (!aligned16(X) || !aligned16(eps) || !aligned16(out) || !aligned16(ws) ||
+      !aligned16(p->W_v) || !aligned16(p->W_o) || !aligned16(p->W_1) || !aligned16(p->W_2))
+    return SP_EINVAL;
+  if (out == X || out == eps) return SP_EINVAL;
+  const GateWs w = gate_ws_layout(dims, T);
+  if (ws_bytes < w.total) return SP_EWORKSPACE;
+  char* base = static_cast<char*>(ws);
+  DenoiseArgs a;
+  a.T = T;
+  a.d = dims->d;
+  a.X = static_cast<const uint16_t*>(X);
+  a.alpha = alpha;
+  a.eps = static_cast<const uint16_t*>(eps);
+  a.ln1_g = p->ln1_g;
+  a.ln1_b = p->ln1_b;
+  a.W_v = static_cast<const uint16_t*>(p->W_v);
+  a.b_v = p->b_v;
+  a.W_o = static_cast<const uint16_t*>(p->W_o);
+  a.b_o = p->b_o;
+  a.ln2_g = p->ln2_g;
+  a.ln2_b = p->ln2_b;
+  a.W_1 = static_cast<const uint16_t*>(p->W_1);
+  a.b_1 = p->b_1;
+  a.W_2 = static_cast<const uint16_t*>(p->W_2);
+  a.b_2 = p->b_2;
+  a.out = static_cast<uint16_t*>(out);
+  a.xt = reinterpret_cast<float*>(base + w.xt);
+  a.buf_p = reinterpret_cast<uint16_t*>(base + w.p);
+  a.buf_q = reinterpret_cast<uint16_t*>(base + w.q);
+  a.hid = reinterpret_cast<uint16_t*>(base + w.hid);
+  record_event(events, 0, stream);
+  const hipError_t e = launch_gate_denoise(a, stream);
+  record_event(events, 1, stream);
+  return hip_status(e);
 }
 
 }  // extern "C"

@@ -455,6 +455,19 @@ __global__ __launch_bounds__(64 * kProjWaves) void project_gemm_bf16_kernel(
   }
 }
 
+// A plain bfloat16 product C = A B^T (bfloat16 out) on the 256 x 256 core,
+// tiles in XCD-grouped order.
+__global__ __launch_bounds__(64 * kProjWaves) void dense_bf16_kernel(DenseRows<__bf16> ar,
+                                                                    DenseRows<__bf16> br,
+                                                                    int64_t M, int64_t N, int K,
+                                                                    uint16_t* C) {
+  __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes];
+  const int64_t nt = (N + kBN - 1) / kBN;
+  const int64_t t = xcd_tile(blockIdx.x, ((M + kBM - 1) / kBM) * nt);
+  if (t < 0) return;
+  gemm_bf16_256<kProjWaves, uint16_t>(ar, br, M, N, K, C, N, (t / nt) * kBM, (t % nt) * kBN, smem);
+}
+
 // grid.x: output tiles, grid.y: K split p, which covers k in [p K, (p + 1) K)
 // and writes partial product p at C + p M N.
 template <typename T, int BM, int BN, int BK>
@@ -793,6 +806,17 @@ hipError_t launch_gram_gemm(const GramArgs& a, hipStream_t stream) {
     hipLaunchKernelGGL(gram_gemm_f32_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, a,
                        per_group, xcd_grouped);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_dense_bf16(const void* A, const void* B, int64_t M, int64_t N, int K, void* C,
+                             hipStream_t stream) {
+  if (M == 0 || N == 0) return hipSuccess;
+  DenseRows<__bf16> ar{(const __bf16*)A, K};
+  DenseRows<__bf16> br{(const __bf16*)B, K};
+  const int64_t blocks = ceil_div(ceil_div(M, kBM) * ceil_div(N, kBN), 8) * 8;
+  hipLaunchKernelGGL(dense_bf16_kernel, dim3((unsigned)blocks), dim3(64 * kProjWaves), 0, stream,
+                     ar, br, M, N, K, (uint16_t*)C);
   return hipGetLastError();
 }
 

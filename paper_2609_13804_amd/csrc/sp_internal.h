@@ -147,4 +147,39 @@ struct CompactArgs {
 };
 hipError_t launch_compact(const CompactArgs& a, hipStream_t stream);
 
+// C = A B^T for bfloat16 A [M, K] and B [N, K] (rows K-contiguous), bfloat16
+// C [M, N]; K a multiple of 32.
+hipError_t launch_dense_bf16(const void* A, const void* B, int64_t M, int64_t N, int K, void* C,
+                             hipStream_t stream);
+
+// Noise gate and locally masked denoiser (denoise.hip).  Workspace buffers:
+// xt float32 [T, d] (the residual stream), buf_p and buf_q bfloat16 [T, d],
+// hid bfloat16 [T, 4d].
+constexpr float kDenoiseLnEps = 1e-6f;
+struct DenoiseArgs {
+  int64_t T;
+  int d;
+  const uint16_t* X;
+  const float* alpha;
+  const uint16_t* eps;
+  const float* ln1_g;
+  const float* ln1_b;
+  const uint16_t* W_v;
+  const float* b_v;
+  const uint16_t* W_o;
+  const float* b_o;
+  const float* ln2_g;
+  const float* ln2_b;
+  const uint16_t* W_1;
+  const float* b_1;
+  const uint16_t* W_2;
+  const float* b_2;
+  uint16_t* out;
+  float* xt;
+  uint16_t* buf_p;
+  uint16_t* buf_q;
+  uint16_t* hid;
+};
+hipError_t launch_gate_denoise(const DenoiseArgs& a, hipStream_t stream);
+
 }  // namespace sp

@@ -293,6 +293,41 @@ def make_inputs(w: Workload, images: Optional[List[int]] = None) -> Dict[str, np
     return out
 
 
+STREAM_DENOISER = 5
+DENOISER_FIELDS = ("ln1_g", "ln1_b", "W_v", "b_v", "W_o", "b_o", "ln2_g", "ln2_b", "W_1", "b_1",
+                   "W_2", "b_2")
+
+
+def make_denoiser_inputs(w: Workload, T: int) -> Dict[str, np.ndarray]:
+    """Seeded inputs of the noise gate and denoiser block for T tokens of width
+    w.d: gate weights alpha ~ U[0, 1] (the first two tokens get exactly 1 and
+    0), noise eps ~ N(0, I) rounded to bfloat16, random-init block parameters
+    (weights N(0, 1/fan_in) rounded to bfloat16 in [out, in] layout, biases
+    N(0, 0.02^2), LayerNorm scales 1 + N(0, 0.1^2) and shifts N(0, 0.1^2),
+    float32)."""
+    d = w.d
+    rng = _rng(w.cfg_id, STREAM_DENOISER, 0)
+    bf = lambda a: _to_dtype_values(a, "bf16")
+    out = {"alpha": rng.uniform(0.0, 1.0, T).astype(np.float32),
+           "eps": bf(rng.standard_normal((T, d), dtype=np.float32))}
+    if T >= 2:
+        out["alpha"][:2] = (1.0, 0.0)
+    shapes = {"W_v": (d, d), "W_o": (d, d), "W_1": (4 * d, d), "W_2": (d, 4 * d)}
+    for name in DENOISER_FIELDS:
+        if name in shapes:
+            n_out, n_in = shapes[name]
+            out[name] = bf(rng.standard_normal((n_out, n_in), dtype=np.float32)
+                           * np.float32(1.0 / math.sqrt(n_in)))
+        elif name.startswith("ln") and name.endswith("_g"):
+            out[name] = (1.0 + 0.1 * rng.standard_normal(d)).astype(np.float32)
+        elif name.startswith("ln"):
+            out[name] = (0.1 * rng.standard_normal(d)).astype(np.float32)
+        else:
+            n = 4 * d if name == "b_1" else d
+            out[name] = (0.02 * rng.standard_normal(n)).astype(np.float32)
+    return out
+
+
 def load_stop_bias() -> Dict[str, float]:
     if not os.path.exists(STOP_BIAS_FILE):
         return {}

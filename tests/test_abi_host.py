@@ -50,7 +50,10 @@ def test_workspace_bytes(sp):
     assert sel >= 256 + 3 * 2 * 51 * 52 * 4
     assert sp.stepprune_workspace_bytes(2, dm, 100, 10, 2, 3, 50, 10) == 256
     assert sp.stepprune_workspace_bytes(1, dm, 100, 10, 2, 3, 5000, 10) == 0   # group too large
-    assert sp.stepprune_workspace_bytes(3, dm, 100, 10, 2, 3, 50, 10) == 0
+    gate = sp.stepprune_workspace_bytes(3, dm, 100, 10, 2, 3, 50, 10)   # T = 100 tokens, d = 256
+    assert gate >= 256 + 100 * 256 * (4 + 2 + 2 + 8)
+    assert sp.stepprune_workspace_bytes(3, _dims(sp, dtype=sp.SP_F32), 100, 10, 2, 3, 50, 10) == 0
+    assert sp.stepprune_workspace_bytes(4, dm, 100, 10, 2, 3, 50, 10) == 0
     assert sp.stepprune_workspace_bytes(0, _dims(sp, h=100), 100, 10, 2, 3, 50, 10) == 0
 
 
@@ -107,6 +110,29 @@ def _select_traj(sp, traj, **kw):
                 traj=traj, ws=FAKE, ws_bytes=0)
     args.update(kw)
     return sp.stepprune_select_trajectory(_dims(sp), stream=0, raise_on_error=False, **args)
+
+
+def test_gate_denoise_validation(sp):
+    names = ["ln1_g", "ln1_b", "W_v", "b_v", "W_o", "b_o", "ln2_g", "ln2_b", "W_1", "b_1",
+             "W_2", "b_2"]
+    full = sp.sp_denoiser(**{n: FAKE for n in names})
+    dm = _dims(sp)
+    ws_bytes = sp.stepprune_workspace_bytes(3, dm, 10, 0, 1, 0, 0, 0)
+
+    def call(dm=dm, X=FAKE, T=10, alpha=FAKE, eps=FAKE, p=full, out=FAKE + 0x100000, ws=FAKE,
+             ws_bytes=ws_bytes):
+        return sp.stepprune_gate_denoise(dm, X, T, alpha, eps, p, out, ws, ws_bytes, stream=0,
+                                         raise_on_error=False)
+    assert call(dm=_dims(sp, dtype=sp.SP_F32)) == sp.SP_EUNSUPPORTED
+    assert call(dm=_dims(sp, d=4160, dt=4160)) == sp.SP_EUNSUPPORTED
+    assert call(T=-1) == sp.SP_EINVAL
+    assert call(X=None) == sp.SP_EINVAL
+    assert call(out=FAKE) == sp.SP_EINVAL                  # aliases X
+    assert call(X=MISALIGNED) == sp.SP_EINVAL
+    assert call(ws_bytes=ws_bytes - 1) == sp.SP_EWORKSPACE
+    for n in names:
+        part = sp.sp_denoiser(**{m: (None if m == n else FAKE) for m in names})
+        assert call(p=part) == sp.SP_EINVAL, n
 
 
 def test_select_trajectory_validation(sp):

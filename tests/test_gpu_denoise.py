@@ -1,0 +1,102 @@
+"""The noise gate (Eq. 9) and locally masked denoiser on the GPU
+(stepprune_gate_denoise) against the oracle (oracle/denoise.py, mirror mode:
+bfloat16 roundings where the GPU stores bfloat16).
+
+The block is per token, so the oracle can compute any subset of rows: small
+batches are checked on every row, the full 9216 x 4096 batch on sampled rows
+(always including the gate's end points, a = 1 and a = 0, and the last row).
+
+Tolerance.  Both sides round the same values to bfloat16 at the same six
+points; the GPU computes in float32 between them and the oracle in float64,
+so a value that lies within float32 error of a rounding boundary can round to
+the neighbouring bfloat16 (one ulp, 2^-8 relative) on one side, and such a
+flip propagates through the products that follow.  Per row the normwise
+relative error is therefore a small multiple of 2^-9: the bound is 1e-2, and
+most outputs must be bit-identical.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_13804_amd import binding as sp
+from paper_2609_13804_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+ROW_TOL = 1e-2
+MIN_EQUAL = 0.6
+
+
+def _run(w, T, rows=None):
+    """GPU output for the first T visual rows of workload w, and its inputs."""
+    X = W.make_inputs(w)["X"][:T] if T <= W.make_layout(w).img_off[-1] else None
+    assert X is not None and X.shape[0] == T
+    inp = W.make_denoiser_inputs(w, T)
+    dev = torch.device("cuda")
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev, torch.bfloat16)
+    f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+    t = {k: (bf(v) if k.startswith("W_") else f32(v)) for k, v in inp.items()
+         if k in W.DENOISER_FIELDS}
+    Xd, eps, alpha = bf(X), bf(inp["eps"]), f32(inp["alpha"])
+    dm = sp.dims(w.d, w.d_text, w.h, sp.SP_BF16)
+    ws_bytes = sp.stepprune_workspace_bytes(sp.STAGE_GATE, dm, T, 0, 1, 0, 0, 0)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device=dev)
+    out = torch.empty((T, w.d), dtype=torch.bfloat16, device=dev)
+    params = sp.denoiser(**t)
+    sp.stepprune_gate_denoise(dm, Xd, T, alpha, eps, params, out, ws, ws_bytes)
+    torch.cuda.synchronize()
+    assert sp.stepprune_read_device_error(ws) == 0
+    return out.float().cpu().numpy().astype(np.float64), X, inp
+
+
+def _oracle_rows(X, inp, rows):
+    p = oracle.DenoiserParams(**{k: np.asarray(inp[k], np.float64) for k in W.DENOISER_FIELDS})
+    return oracle.gate_denoise(X[rows], inp["alpha"][rows], inp["eps"][rows], p, mirror=True)
+
+
+def _check(got, want):
+    rel = np.linalg.norm(got - want, axis=1) / np.linalg.norm(want, axis=1)
+    equal = np.mean(got == want)
+    print(f"rows {got.shape[0]}: max row error {rel.max():.2e}, mean {rel.mean():.2e}, "
+          f"bit-equal {equal:.3f}", flush=True)
+    assert np.all(np.isfinite(got))
+    assert rel.max() <= ROW_TOL
+    assert equal >= MIN_EQUAL
+
+
+@pytest.mark.parametrize("name,T", [("tiny_bf16", 200), ("mid_bf16", 700)])
+def test_gate_denoise_every_row(gpu_lib, name, T):
+    w = W.WORKLOADS[name]
+    got, X, inp = _run(w, T)
+    rows = np.arange(T)
+    want = _oracle_rows(X, inp, rows)
+    _check(got, want)
+    # a = 1 keeps the token and a = 0 replaces it by noise before the block:
+    # rows 0 and 1 equal the block applied to x_0 and to eps_1
+    p = oracle.DenoiserParams(**{k: np.asarray(inp[k], np.float64) for k in W.DENOISER_FIELDS})
+    np.testing.assert_array_equal(want[0], oracle.denoise(X[:1].astype(np.float64), p)[0])
+    np.testing.assert_array_equal(want[1], oracle.denoise(inp["eps"][1:2].astype(np.float64), p)[0])
+
+
+def test_gate_denoise_full_size_sampled_rows(gpu_lib):
+    w = W.WORKLOADS["llava15_bf16"]
+    T = int(W.make_layout(w).img_off[-1])
+    got, X, inp = _run(w, T)
+    rng = np.random.default_rng(2609)
+    rows = np.unique(np.concatenate([[0, 1, T - 1], rng.choice(T, 45, replace=False)]))
+    _check(got[rows], _oracle_rows(X, inp, rows))
+
+
+def test_gate_denoise_no_tokens(gpu_lib):
+    w = W.WORKLOADS["tiny_bf16"]
+    dm = sp.dims(w.d, w.d_text, w.h, sp.SP_BF16)
+    dev = torch.device("cuda")
+    inp = W.make_denoiser_inputs(w, 2)
+    t = {k: torch.from_numpy(np.asarray(v)).to(dev) for k, v in inp.items() if k in W.DENOISER_FIELDS}
+    ws_bytes = sp.stepprune_workspace_bytes(sp.STAGE_GATE, dm, 0, 0, 1, 0, 0, 0)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device=dev)
+    out = torch.empty((1, w.d), dtype=torch.bfloat16, device=dev)
+    assert sp.stepprune_gate_denoise(dm, None, 0, None, None, sp.denoiser(**t), out, ws,
+                                     ws_bytes) == sp.SP_OK
+    torch.cuda.synchronize()
