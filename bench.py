@@ -27,7 +27,7 @@ GPU reaches on library work; "cpu_baseline" is the float64 oracle timed on this
 host's cores over a bounded sample of the same batch.
 
     python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--streams 3] [--slots 4]
-                    [--workload llava15_bf16] [--trajectory TAU BETA] [--steady R]
+                    [--workload llava15_bf16] [--trajectory TAU BETA] [--steady R] [--denoise]
 """
 import argparse
 import ctypes
@@ -197,6 +197,50 @@ def steady_pass(w, R, b_stop, hip, stream, t_scan_roof, ref_kept, steps=10, warm
             "frac_keyscan_roofline": round(R * t_scan_roof / (sel * 1e-6), 4),
             "note": "secondary figure: R copies of the batch per call of each stage; "
                     "not the headline value"}
+
+
+def gate_denoise_pass(w, K, hip, stream, mfma_peak):
+    """The training pathway's noise gate and masked denoiser (stepprune_gate_denoise)
+    on the batch's visual tokens: mean time of the whole block over K calls
+    (HIP events around it) and its matrix throughput; 20 T d^2 flop (value and
+    output projections, the 4d MLP)."""
+    import numpy as np
+    import torch
+    from paper_2609_13804_amd import binding as sp
+    from paper_2609_13804_amd import workloads as W
+    T = int(W.make_layout(w).img_off[-1])
+    dev = torch.device("cuda")
+    inp = W.make_denoiser_inputs(w, T)
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev, torch.bfloat16)
+    f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+    t = {k: (bf(v) if k.startswith("W_") else f32(v)) for k, v in inp.items()
+         if k in W.DENOISER_FIELDS}
+    X = bf(W.make_inputs(w)["X"])
+    eps, alpha = bf(inp["eps"]), f32(inp["alpha"])
+    del inp
+    dm = sp.dims(w.d, w.d_text, w.h, sp.SP_BF16)
+    ws_bytes = sp.stepprune_workspace_bytes(sp.STAGE_GATE, dm, T, 0, 1, 0, 0, 0)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device=dev)
+    out = torch.empty((T, w.d), dtype=torch.bfloat16, device=dev)
+    params = sp.denoiser(**t)
+    for _ in range(3):
+        sp.stepprune_gate_denoise(dm, X, T, alpha, eps, params, out, ws, ws_bytes, stream)
+    evs = [(hip.create(), hip.create()) for _ in range(K)]
+    for e in evs:
+        sp.stepprune_gate_denoise(dm, X, T, alpha, eps, params, out, ws, ws_bytes, stream,
+                                  events=[e[0], e[1]])
+    torch.cuda.synchronize()
+    if sp.stepprune_read_device_error(ws):
+        raise RuntimeError("device error in the gate and denoiser")
+    us = float(np.mean([1e3 * hip.ms(a, b) for a, b in evs]))
+    for a, b in evs:
+        hip.destroy(a)
+        hip.destroy(b)
+    flop = 20.0 * T * w.d * w.d
+    achieved = flop / (us * 1e-6) / 1e12
+    return {"tokens": T, "d": w.d, "us": round(us, 2), "algorithmic": f"{flop * 1e-12:.4f} TFLOP",
+            "achieved_tflops": round(achieved, 2), "frac": round(achieved / mfma_peak, 4),
+            "bound": "mfma"}
 
 
 def host_info():
@@ -373,6 +417,9 @@ def main(argv=None):
     ap.add_argument("--steady", type=int, default=0, metavar="R",
                     help="also time the selection stage on R copies of the batch in one call "
                          "(R x the episodes at once): a secondary steady-state figure")
+    ap.add_argument("--denoise", action="store_true",
+                    help="also time the training pathway's noise gate and masked denoiser "
+                         "(stepprune_gate_denoise) on the batch's visual tokens")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle work for the CPU baseline sample")
@@ -636,6 +683,13 @@ def main(argv=None):
     }
     if args.trajectory is not None:
         out["trajectory"] = trajectory_pass(run, args.trajectory, K, hip)
+    if args.denoise:
+        if w.dtype != "bf16":
+            raise SystemExit("--denoise needs a bfloat16 workload")
+        out["gate_denoise"] = gate_denoise_pass(w, K, hip, stream, mfma_peak)
+        if peaks.get("bf16_matmul_TFLOPs"):
+            out["gate_denoise"]["frac_measured_peak"] = round(
+                out["gate_denoise"]["achieved_tflops"] / peaks["bf16_matmul_TFLOPs"], 4)
     if args.steady > 0:
         out["select_steady"] = steady_pass(w, args.steady, b_stop, hip, stream, t_scan_roof,
                                            run.kept_lists())

@@ -287,7 +287,8 @@ sp_status stepprune_compact(const sp_dims* dims,
  * input here; eps holds the caller's N(0, 1) draws.
  *
  * bfloat16 only (SP_EUNSUPPORTED otherwise).  Weights use the [out, in]
- * layout; vectors are float32.  The residual stream is float32; every product
+ * layout; vectors are float32.  Every array is 16-byte aligned (SP_EINVAL
+ * otherwise).  The residual stream is float32; every product
  * operand and result is rounded once to bfloat16.  d <= 4096.
  */
 typedef struct {

@@ -314,7 +314,9 @@ sp_status stepprune_gate_denoise(const sp_dims* dims, const void* X, int64_t T,
       !p->ln2_b || !p->W_1 || !p->b_1 || !p->W_2 || !p->b_2)
     return SP_EINVAL;
   if (!aligned16(X) || !aligned16(eps) || !aligned16(out) || !aligned16(ws) ||
-      !aligned16(p->W_v) || !aligned16(p->W_o) || !aligned16(p->W_1) || !aligned16(p->W_2))
+      !aligned16(p->W_v) || !aligned16(p->W_o) || !aligned16(p->W_1) || !aligned16(p->W_2) ||
+      !aligned16(p->ln1_g) || !aligned16(p->ln1_b) || !aligned16(p->b_v) || !aligned16(p->b_o) ||
+      !aligned16(p->ln2_g) || !aligned16(p->ln2_b) || !aligned16(p->b_1) || !aligned16(p->b_2))
     return SP_EINVAL;
   if (out == X || out == eps) return SP_EINVAL;
   const GateWs w = gate_ws_layout(dims, T);

@@ -130,6 +130,8 @@ def test_gate_denoise_validation(sp):
     assert call(out=FAKE) == sp.SP_EINVAL                  # aliases X
     assert call(X=MISALIGNED) == sp.SP_EINVAL
     assert call(ws_bytes=ws_bytes - 1) == sp.SP_EWORKSPACE
+    assert call(p=sp.sp_denoiser(**{m: (MISALIGNED if m == "b_1" else FAKE) for m in names})) \
+        == sp.SP_EINVAL
     for n in names:
         part = sp.sp_denoiser(**{m: (None if m == n else FAKE) for m in names})
         assert call(p=part) == sp.SP_EINVAL, n
