@@ -13,6 +13,10 @@
  *                      episode, kept indices restored to native order;
  *   stepprune_compact  step 5: physical gather of the kept tokens ahead of the
  *                      prompt into a padded or packed prefill buffer.
+ * Beside them, for the training pathway (Section "Trajectory-Aware
+ * Differentiable Optimization"): stepprune_select_trajectory (the trajectory
+ * sums of Eqs. 5-7) and stepprune_gate_denoise (the noise gate of Eq. 9 and
+ * the locally masked denoiser).
  *
  * Conventions shared by every call
  *  - Pointers are DEVICE pointers unless marked (host).  All row-major.
