@@ -25,8 +25,9 @@
  *  - Every call validates its host-side arguments first and returns a status
  *    before launching anything.  On SP_OK the work is enqueued on `stream` and
  *    the call returns; outputs are valid once the stream has been synchronised.
- *  - The library allocates no memory and keeps no state besides kernel handles.
- *    The caller owns every buffer, including the workspace `ws` whose size
+ *  - The library allocates no memory and keeps no state besides kernel handles
+ *    and the fixed device scratch of stepprune_select_noalloc.  The caller owns
+ *    every buffer, including the workspace `ws` whose size
  *    stepprune_workspace_bytes() gives; a workspace may be reused by later calls
  *    on the same stream.
  *  - Errors that depend on device-resident data (inconsistent offsets, a group
@@ -201,6 +202,45 @@ sp_status stepprune_select(const sp_dims* dims,
                            float* trace, int32_t trace_steps,
                            void* ws, size_t ws_bytes,
                            const hipEvent_t* events, hipStream_t stream);
+
+/*
+ * stepprune_select for callers that cannot allocate device memory (code under
+ * HIP graph capture, serving loops or harnesses that forbid allocation): the
+ * same selection, decisions and outputs, with no caller workspace.  The
+ * scratch (the Gram blocks, the context split and the group-local kept lists
+ * that stepprune_select keeps in `ws`) is a fixed array of
+ * STEPPRUNE_NOALLOC_SCRATCH_BYTES in the library's device memory, one copy per
+ * GPU, held until the process ends.  The call itself allocates nothing; its
+ * first call on a GPU looks up that GPU's copy.
+ *
+ * Arguments as for stepprune_select, without ws / ws_bytes, plus
+ *  err   out  device pointer to a caller-owned, 4-byte-aligned int32 error
+ *             word, zero before the first call; it plays the role of the
+ *             workspace's error word (the first SP_DEV_* code sticks until
+ *             stepprune_read_device_error(err, ...) reads and clears it).
+ *  stream     must belong to the current device (SP_EINVAL otherwise).
+ * Sizes whose stepprune_workspace_bytes(1, ...) exceeds
+ * STEPPRUNE_NOALLOC_SCRATCH_BYTES return SP_EWORKSPACE before any launch
+ * (64 MiB holds, for example, 24 groups of 576 tokens at h = 1024).
+ * Every call on a GPU uses that GPU's one array, which keeps the last call's
+ * contents: calls that overlap on one GPU (different streams, or several
+ * host threads) race and must be serialised by the caller.  SP_REUSE_GRAM
+ * reads the Gram products that the last SP_GRAM_ONLY call on the GPU left
+ * there.
+ */
+#define STEPPRUNE_NOALLOC_SCRATCH_BYTES (64u << 20)
+sp_status stepprune_select_noalloc(const sp_dims* dims,
+                                   const void* KQV, const float* ctx, int64_t T_vis,
+                                   const int32_t* img_off, int32_t B,
+                                   const int32_t* grp_off, const int32_t* grp_img,
+                                   const int32_t* grp_cap, int32_t G,
+                                   int32_t max_group, int32_t max_cap,
+                                   const int32_t* kept_off,
+                                   float b_stop, int32_t g, uint32_t flags,
+                                   int32_t* kept_idx, int32_t* kept_cnt, int32_t* grp_cnt,
+                                   float* trace, int32_t trace_steps,
+                                   int32_t* err,
+                                   const hipEvent_t* events, hipStream_t stream);
 
 /*
  * Trajectory sums of the training surrogate (Section "Trajectory-Aware

@@ -22,7 +22,9 @@ STAGE_PROJECT, STAGE_SELECT, STAGE_COMPACT = 0, 1, 2
 
 EXPORTS = ["stepprune_project", "stepprune_select", "stepprune_select_trajectory", "stepprune_compact",
            "stepprune_gate_denoise", "stepprune_workspace_bytes", "stepprune_read_device_error",
-           "stepprune_status_string"]
+           "stepprune_status_string", "stepprune_select_noalloc"]
+# size of the fixed device scratch of stepprune_select_noalloc (per GPU)
+NOALLOC_SCRATCH_BYTES = 64 << 20
 STAGE_GATE = 3
 
 
@@ -65,6 +67,10 @@ _lib.stepprune_project.argtypes = [_DIMS, _P, _I64, _P, _P, _P, _P, _P, _I32, _I
 _lib.stepprune_select.restype = _I32
 _lib.stepprune_select.argtypes = [_DIMS, _P, _P, _I64, _P, _I32, _P, _P, _P, _I32, _I32, _I32, _P,
                                   _F32, _I32, ctypes.c_uint32, _P, _P, _P, _P, _I32, _P, _SZ, _P, _P]
+_lib.stepprune_select_noalloc.restype = _I32
+_lib.stepprune_select_noalloc.argtypes = [_DIMS, _P, _P, _I64, _P, _I32, _P, _P, _P, _I32, _I32, _I32,
+                                          _P, _F32, _I32, ctypes.c_uint32, _P, _P, _P, _P, _I32, _P,
+                                          _P, _P]
 _lib.stepprune_select_trajectory.restype = _I32
 _lib.stepprune_select_trajectory.argtypes = [_DIMS, _P, _P, _I64, _P, _I32, _P, _P, _P, _I32, _I32,
                                              _I32, _P, _F32, _I32, ctypes.c_uint32, _P, _P, _P, _P,
@@ -150,6 +156,18 @@ def stepprune_select(dm, KQV, ctx, T_vis, img_off, B, grp_off, grp_img, grp_cap,
                                _ptr(grp_cnt), _ptr(trace), trace_steps, _ptr(ws), ws_bytes,
                                _events(events), _stream(stream))
     return _check("stepprune_select", st, raise_on_error)
+
+
+def stepprune_select_noalloc(dm, KQV, ctx, T_vis, img_off, B, grp_off, grp_img, grp_cap, G,
+                             max_group, max_cap, kept_off, b_stop, g, flags, kept_idx, kept_cnt,
+                             grp_cnt, trace, trace_steps, err, stream=None, raise_on_error=True,
+                             events=None):
+    st = _lib.stepprune_select_noalloc(ctypes.byref(dm), _ptr(KQV), _ptr(ctx), T_vis, _ptr(img_off),
+                                       B, _ptr(grp_off), _ptr(grp_img), _ptr(grp_cap), G, max_group,
+                                       max_cap, _ptr(kept_off), b_stop, g, flags, _ptr(kept_idx),
+                                       _ptr(kept_cnt), _ptr(grp_cnt), _ptr(trace), trace_steps,
+                                       _ptr(err), _events(events), _stream(stream))
+    return _check("stepprune_select_noalloc", st, raise_on_error)
 
 
 def trajectory(tau, beta, s, kbar, pstop=None, pstop_steps=0) -> sp_trajectory:

@@ -3,6 +3,8 @@
 // touching the device and never throws.
 #include <string.h>
 
+#include <mutex>
+
 #include "sp_internal.h"
 
 using namespace sp;
@@ -137,8 +139,42 @@ sp_status stepprune_project(const sp_dims* dims, const void* X, int64_t T_vis, c
 
 namespace {
 
-// Shared body of stepprune_select and stepprune_select_trajectory (traj may be
-// null for the former).
+// ------------------------------------------------------------ fixed scratch
+// The scratch of stepprune_select_noalloc: one array in device memory, a copy
+// per GPU, held until the process ends.  In host code the array's name is a
+// stand-in, not a device address: host code uses only the address that
+// hipGetSymbolAddress returns for the current device, fetched once per device
+// and kept in scratch_ptr.
+static __device__ __align__(256) char scratch[STEPPRUNE_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void* scratch_ptr[kMaxDevices];
+
+// The scratch address on the device that owns `stream` (it must be the
+// current device: the symbol is looked up with that device current).
+sp_status device_scratch(hipStream_t stream, void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return SP_EHIP;
+  if (stream) {
+    hipDevice_t sdev = -1;
+    if (hipStreamGetDevice(stream, &sdev) != hipSuccess) return SP_EHIP;
+    if (sdev != dev) return SP_EINVAL;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return SP_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return SP_EHIP;
+    scratch_ptr[dev] = p;
+  }
+  *out = scratch_ptr[dev];
+  return SP_OK;
+}
+
+// Shared body of stepprune_select, stepprune_select_trajectory (traj may be
+// null for the others) and stepprune_select_noalloc (use_scratch: the
+// workspace is the device's fixed scratch and the error word is err_word).
 sp_status select_impl(const sp_dims* dims, const void* KQV, const float* ctx, int64_t T_vis,
                       const int32_t* img_off, int32_t B, const int32_t* grp_off,
                       const int32_t* grp_img, const int32_t* grp_cap, int32_t G,
@@ -146,7 +182,8 @@ sp_status select_impl(const sp_dims* dims, const void* KQV, const float* ctx, in
                       int32_t g, uint32_t flags, int32_t* kept_idx, int32_t* kept_cnt,
                       int32_t* grp_cnt, float* trace, int32_t trace_steps,
                       const sp_trajectory* traj, void* ws, size_t ws_bytes,
-                      const hipEvent_t* events, hipStream_t stream) {
+                      const hipEvent_t* events, hipStream_t stream,
+                      bool use_scratch = false, int32_t* err_word = nullptr) {
   sp_status st = check_dims(dims);
   if (st != SP_OK) return st;
   if (T_vis < 0 || B < 1 || G < 0 || max_group < 0 || max_cap < 0 || trace_steps < 0)
@@ -158,7 +195,9 @@ sp_status select_impl(const sp_dims* dims, const void* KQV, const float* ctx, in
     return SP_EINVAL;
   if ((flags & SP_GRAM_ONLY) && (flags & SP_REUSE_GRAM)) return SP_EINVAL;
   if ((flags & SP_GRAM_ONLY) && traj) return SP_EINVAL;
-  if (!KQV || !ctx || !img_off || !kept_off || !kept_cnt || !ws) return SP_EINVAL;
+  if (!KQV || !ctx || !img_off || !kept_off || !kept_cnt) return SP_EINVAL;
+  if (use_scratch ? !err_word || (reinterpret_cast<uintptr_t>(err_word) & 3u) : !ws)
+    return SP_EINVAL;
   if (G > 0 && (!grp_off || !grp_img || !grp_cap || !kept_idx)) return SP_EINVAL;
   if ((flags & SP_TRACE) && trace_steps > 0 && !trace) return SP_EINVAL;
   if (b_stop != b_stop) return SP_EINVAL;   // NaN
@@ -168,8 +207,14 @@ sp_status select_impl(const sp_dims* dims, const void* KQV, const float* ctx, in
     if ((G > 0 && !traj->kbar) || (T_vis > 0 && !traj->s)) return SP_EINVAL;
     if (g != 1) return SP_EUNSUPPORTED;
   }
-  if (!aligned16(KQV) || !aligned16(ctx) || !aligned16(ws)) return SP_EINVAL;
+  if (!aligned16(KQV) || !aligned16(ctx) || (!use_scratch && !aligned16(ws))) return SP_EINVAL;
   const SelectWs lay = select_ws_layout(dims, B, G, max_group, max_cap);
+  if (use_scratch) {
+    if (lay.total > (size_t)STEPPRUNE_NOALLOC_SCRATCH_BYTES) return SP_EWORKSPACE;
+    const sp_status sst = device_scratch(stream, &ws);
+    if (sst != SP_OK) return sst;
+    ws_bytes = STEPPRUNE_NOALLOC_SCRATCH_BYTES;
+  }
   if (ws_bytes < lay.total) return SP_EWORKSPACE;
 
   char* wsb = static_cast<char*>(ws);
@@ -208,7 +253,7 @@ sp_status select_impl(const sp_dims* dims, const void* KQV, const float* ctx, in
   a.csplit = wsb + lay.csplit;
   a.grp_kept = reinterpret_cast<int32_t*>(wsb + lay.kept);
   a.grp_count = reinterpret_cast<int32_t*>(wsb + lay.count);
-  a.err = reinterpret_cast<int32_t*>(wsb);
+  a.err = use_scratch ? err_word : reinterpret_cast<int32_t*>(wsb);
   a.events = events;
   return hip_status(launch_select(a, stream));
 }
@@ -244,6 +289,20 @@ sp_status stepprune_select_trajectory(const sp_dims* dims, const void* KQV, cons
   return select_impl(dims, KQV, ctx, T_vis, img_off, B, grp_off, grp_img, grp_cap, G, max_group,
                      max_cap, kept_off, b_stop, g, flags, kept_idx, kept_cnt, grp_cnt, trace,
                      trace_steps, traj, ws, ws_bytes, events, stream);
+}
+
+sp_status stepprune_select_noalloc(const sp_dims* dims, const void* KQV, const float* ctx,
+                                   int64_t T_vis, const int32_t* img_off, int32_t B,
+                                   const int32_t* grp_off, const int32_t* grp_img,
+                                   const int32_t* grp_cap, int32_t G, int32_t max_group,
+                                   int32_t max_cap, const int32_t* kept_off, float b_stop,
+                                   int32_t g, uint32_t flags, int32_t* kept_idx,
+                                   int32_t* kept_cnt, int32_t* grp_cnt, float* trace,
+                                   int32_t trace_steps, int32_t* err,
+                                   const hipEvent_t* events, hipStream_t stream) {
+  return select_impl(dims, KQV, ctx, T_vis, img_off, B, grp_off, grp_img, grp_cap, G, max_group,
+                     max_cap, kept_off, b_stop, g, flags, kept_idx, kept_cnt, grp_cnt, trace,
+                     trace_steps, nullptr, nullptr, 0, events, stream, true, err);
 }
 
 sp_status stepprune_compact(const sp_dims* dims, const void* X, const int32_t* img_off,

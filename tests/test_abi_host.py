@@ -103,6 +103,36 @@ def test_select_validation(sp):
     assert _select(sp) == sp.SP_EWORKSPACE
 
 
+def _select_noalloc(sp, **kw):
+    args = dict(KQV=FAKE, ctx=FAKE, T_vis=10, img_off=FAKE, B=1, grp_off=FAKE, grp_img=FAKE,
+                grp_cap=FAKE, G=1, max_group=10, max_cap=4, kept_off=FAKE, b_stop=0.0, g=1,
+                flags=0, kept_idx=FAKE, kept_cnt=FAKE, grp_cnt=None, trace=None, trace_steps=0,
+                err=FAKE)
+    args.update(kw)
+    return sp.stepprune_select_noalloc(_dims(sp), stream=0, raise_on_error=False, **args)
+
+
+def test_select_noalloc_validation(sp):
+    """Only calls that host validation refuses: a valid call would reach the
+    device."""
+    assert _select_noalloc(sp, err=None) == sp.SP_EINVAL               # the error word is required
+    assert _select_noalloc(sp, err=FAKE + 2) == sp.SP_EINVAL           # and 4-byte aligned
+    assert _select_noalloc(sp, g=6) == sp.SP_EUNSUPPORTED
+    assert _select_noalloc(sp, KQV=None) == sp.SP_EINVAL
+    assert _select_noalloc(sp, flags=32) == sp.SP_EINVAL
+    # sizes whose workspace exceeds the fixed scratch: 9 groups of 1000 tokens
+    # need 9 x 8.05 MB of Gram blocks
+    dm = _dims(sp)
+    assert sp.stepprune_workspace_bytes(1, dm, 9000, 0, 1, 9, 1000, 8) > sp.NOALLOC_SCRATCH_BYTES
+    assert _select_noalloc(sp, T_vis=9000, G=9, max_group=1000, max_cap=8) == sp.SP_EWORKSPACE
+    # the 16 x 576 batch at h = 1024 fits, with 24 such groups the most
+    big = sp.dims(4096, 4096, 1024, sp.SP_BF16)
+    fits = [G for G in range(1, 40)
+            if sp.stepprune_workspace_bytes(1, big, 576 * G, 64 * G, G, G, 576, 192)
+            <= sp.NOALLOC_SCRATCH_BYTES]
+    assert max(fits) == 24 and fits == list(range(1, 25))
+
+
 def _select_traj(sp, traj, **kw):
     args = dict(KQV=FAKE, ctx=FAKE, T_vis=10, img_off=FAKE, B=1, grp_off=FAKE, grp_img=FAKE,
                 grp_cap=FAKE, G=1, max_group=10, max_cap=4, kept_off=FAKE, b_stop=0.0, g=1,
