@@ -19,6 +19,7 @@ sp_status check_dims(const sp_dims* d) {
   if (d->d % 64 || d->d_text % 64 || d->h % 64) return SP_EINVAL;
   if (d->dtype != SP_F32 && d->dtype != SP_BF16) return SP_EUNSUPPORTED;
   if (d->h > 1024) return SP_EUNSUPPORTED;
+  if (d->dtype == SP_F32 && d->h > 512) return SP_EUNSUPPORTED;
   return SP_OK;
 }
 

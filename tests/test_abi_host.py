@@ -70,6 +70,14 @@ def test_project_validation(sp):
     assert _project(sp, _dims(sp, d=0)) == sp.SP_EINVAL
     assert _project(sp, _dims(sp, dtype=7)) == sp.SP_EUNSUPPORTED
     assert _project(sp, _dims(sp, h=2048)) == sp.SP_EUNSUPPORTED
+    # float32 takes h <= 512; bfloat16 h <= 1024
+    assert _project(sp, _dims(sp, h=576, dtype=sp.SP_F32)) == sp.SP_EUNSUPPORTED
+    assert _project(sp, _dims(sp, h=1024, dtype=sp.SP_F32)) == sp.SP_EUNSUPPORTED
+    assert _project(sp, _dims(sp, h=512, dtype=sp.SP_F32)) == sp.SP_EWORKSPACE
+    assert _project(sp, _dims(sp, h=1024)) == sp.SP_EWORKSPACE
+    assert _select(sp, _dims(sp, h=576, dtype=sp.SP_F32)) == sp.SP_EUNSUPPORTED
+    assert sp.stepprune_workspace_bytes(1, _dims(sp, h=576, dtype=sp.SP_F32), 100, 10, 2, 3, 50,
+                                        10) == 0
     assert _project(sp, X=None) == sp.SP_EINVAL
     assert _project(sp, KQV=None) == sp.SP_EINVAL
     assert _project(sp, W_kqv=MISALIGNED) == sp.SP_EINVAL

@@ -436,3 +436,50 @@ def test_calibrated_bias_reproduces_predicted_counts():
         w, inp, lay, KQV, ctx, b = _pipeline(name)
         res = oracle.select(KQV, ctx, lay.img_off, lay.grp_off, lay.grp_img, lay.grp_cap, b, w.h)
         assert int(res.kept_cnt.sum()) == table[name]["retained_total"]
+
+
+# ---------------------------------------------------------------- near-tie scale
+# The near-tie exemption (relative top-2 margin below 1e-4) divides the gap by
+# max(|top1|, |top2|, rms of the finite candidate logits).  Hand-computed cases;
+# each fails under a plausible slip: an ascending sort, -inf or masked entries in
+# the rms, a scale of |top1| alone (explodes near zero), min instead of max, a
+# signed instead of absolute top value, or the gap taken to the third logit.
+def test_relative_margin_hand_cases():
+    from oracle.selection import _relative_margin
+    inf = np.inf
+    # finite [1, 3, 2]: top1 3, top2 2, rms sqrt(14/3) = 2.160 < 3, so the gap 1 over 3
+    t1, t2, m = _relative_margin(np.array([1.0, 3.0, -inf, 2.0]))
+    assert (t1, t2) == (3.0, 2.0) and m == pytest.approx(1.0 / 3.0, rel=1e-15)
+    # both leaders near zero: the rms of [1e-3, 0, -4] (sqrt(16.000001 / 3)) sets the scale
+    t1, t2, m = _relative_margin(np.array([1e-3, 0.0, -4.0]))
+    assert (t1, t2) == (1e-3, 0.0)
+    assert m == pytest.approx(1e-3 / np.sqrt(16.000001 / 3.0), rel=1e-12)
+    # negative leaders: |top2| = 5 is the scale, gap 1 (rms sqrt(41/2) = 4.528 < 5)
+    t1, t2, m = _relative_margin(np.array([-4.0, -5.0]))
+    assert (t1, t2, m) == (-4.0, -5.0, pytest.approx(0.2, rel=1e-15))
+    # an exact tie has margin 0 whatever the scale; all-zero logits too
+    assert _relative_margin(np.array([2.0, 2.0, 1.0]))[2] == 0.0
+    assert _relative_margin(np.array([0.0, 0.0]))[2] == 0.0
+    # zero scale with distinct values cannot happen; one finite candidate: no second
+    t1, t2, m = _relative_margin(np.array([-inf, 7.0, -inf]))
+    assert (t1, t2, m) == (7.0, -inf, inf)
+    assert _relative_margin(np.array([-inf, -inf])) == (-inf, -inf, inf)
+    # the rms is over the finite entries only: [6, 5] with two masked -> rms sqrt(30.5) = 5.52 < 6
+    assert _relative_margin(np.array([6.0, -inf, 5.0, -inf]))[2] == pytest.approx(1 / 6, rel=1e-15)
+    # a large third value does not enter the gap, only the scale (rms of [1, 0.5, -9] = 5.23)
+    m = _relative_margin(np.array([1.0, 0.5, -9.0]))[2]
+    assert m == pytest.approx(0.5 / np.sqrt(82.25 / 3.0), rel=1e-12)
+
+
+def test_rel_gap_hand_cases():
+    from oracle.selection import _rel_gap
+    inf = np.inf
+    fin = np.array([2.0, 1.0, 0.0])           # rms sqrt(5/3) = 1.291
+    assert _rel_gap(2.0, 1.0, fin) == pytest.approx(0.5, rel=1e-15)      # scale |a| = 2
+    assert _rel_gap(1.0, 2.0, fin) == pytest.approx(-0.5, rel=1e-15)     # signed
+    assert _rel_gap(2.0, -inf, fin) == inf                                # nothing to tie with
+    # near zero: the rms of [0.01, 0, 3, -3] = sqrt(18.0001 / 4) sets the scale
+    fin = np.array([0.01, 0.0, 3.0, -3.0])
+    assert _rel_gap(0.01, 0.0, fin) == pytest.approx(0.01 / np.sqrt(18.0001 / 4.0), rel=1e-12)
+    assert _rel_gap(0.0, 0.0, np.zeros(3)) == 0.0
+    assert _rel_gap(1e-3, 0.0, np.array([])) == pytest.approx(1.0, rel=1e-15)   # scale |a|
