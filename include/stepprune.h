@@ -89,7 +89,10 @@ enum {
      same arguments and workspace runs the recurrence on them.  Between the
      two, KQV, ctx, the offsets and the workspace must not change. */
   SP_GRAM_ONLY = 8u,
-  SP_REUSE_GRAM = 16u
+  SP_REUSE_GRAM = 16u,
+  /* Diagnostic, with SP_TRACE: every trace record is followed by the step's
+     whole logit vector (see stepprune_select's `trace`). */
+  SP_LOGITS = 32u
 };
 
 enum { SP_LAYOUT_PADDED = 0, SP_LAYOUT_PACKED = 1 };
@@ -173,7 +176,7 @@ sp_status stepprune_project(const sp_dims* dims,
  *  b_stop         additive STOP bias (may be +-inf)
  *  g              tokens kept per non-STOP round, 1 <= g <= 5
  *                 (SP_EUNSUPPORTED above 5)
- *  flags          SP_TRACE, SP_NO_HISTORY, SP_FULL_ROLLOUT, SP_GRAM_ONLY or
+ *  flags          SP_TRACE (with SP_LOGITS), SP_NO_HISTORY, SP_FULL_ROLLOUT, SP_GRAM_ONLY or
  *                 SP_REUSE_GRAM (not both; SP_GRAM_ONLY writes none of the
  *                 outputs and is refused by stepprune_select_trajectory)
  *  kept_idx  out  image-local kept indices, ascending per image, at kept_off[b]
@@ -189,6 +192,12 @@ sp_status stepprune_project(const sp_dims* dims,
  *                 taken logit (the STOP logit for STOP), the largest logit
  *                 left out (STOP included when not taken; -inf if none), STOP
  *                 logit}.  Either way records past the end hold -2 in slot 0.
+ *                 With SP_LOGITS (which needs SP_TRACE) each record is
+ *                 followed by max_group + 1 float32: the step's (round's)
+ *                 logit of every token slot 0..max_group-1 (-inf for tokens
+ *                 already selected and for slots past the group), then the
+ *                 STOP logit; records are then 4 + max_group + 1 (g = 1) or
+ *                 g + 3 + max_group + 1 floats wide (-inf past the end).
  */
 sp_status stepprune_select(const sp_dims* dims,
                            const void* KQV, const float* ctx, int64_t T_vis,

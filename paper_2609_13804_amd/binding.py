@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(HERE, "libstepprune.so")
 
 SP_OK, SP_EINVAL, SP_EUNSUPPORTED, SP_EWORKSPACE, SP_EHIP, SP_EDEVICE = range(6)
 SP_F32, SP_BF16 = 0, 1
-SP_TRACE, SP_NO_HISTORY, SP_FULL_ROLLOUT, SP_GRAM_ONLY, SP_REUSE_GRAM = 1, 2, 4, 8, 16
+SP_TRACE, SP_NO_HISTORY, SP_FULL_ROLLOUT, SP_GRAM_ONLY, SP_REUSE_GRAM, SP_LOGITS = 1, 2, 4, 8, 16, 32
 SP_LAYOUT_PADDED, SP_LAYOUT_PACKED = 0, 1
 SP_DEV_OK, SP_DEV_BAD_OFFSETS, SP_DEV_GROUP_TOO_LARGE, SP_DEV_BAD_CAP, SP_DEV_OUTPUT_OVERFLOW = range(5)
 STAGE_PROJECT, STAGE_SELECT, STAGE_COMPACT = 0, 1, 2

@@ -192,8 +192,10 @@ sp_status select_impl(const sp_dims* dims, const void* KQV, const float* ctx, in
   if (g < 1) return SP_EINVAL;
   if (g > kGMax) return SP_EUNSUPPORTED;
   if (max_group > kMaxGroup) return SP_EUNSUPPORTED;
-  if (flags & ~(uint32_t)(SP_TRACE | SP_NO_HISTORY | SP_FULL_ROLLOUT | SP_GRAM_ONLY | SP_REUSE_GRAM))
+  if (flags & ~(uint32_t)(SP_TRACE | SP_NO_HISTORY | SP_FULL_ROLLOUT | SP_GRAM_ONLY | SP_REUSE_GRAM |
+                          SP_LOGITS))
     return SP_EINVAL;
+  if ((flags & SP_LOGITS) && !(flags & SP_TRACE)) return SP_EINVAL;
   if ((flags & SP_GRAM_ONLY) && (flags & SP_REUSE_GRAM)) return SP_EINVAL;
   if ((flags & SP_GRAM_ONLY) && traj) return SP_EINVAL;
   if (!KQV || !ctx || !img_off || !kept_off || !kept_cnt) return SP_EINVAL;

@@ -56,6 +56,9 @@ struct SelParams {
   int32_t* grp_cnt_out;
   float* trace;
   int trace_steps;
+  int trace_w;         // floats per trace record
+  int logit_off;       // SP_LOGITS: offset of the logit vector in a record
+  int logit_n;         // SP_LOGITS: token slots of that vector (max_group; 0 = no dump)
   // trajectory sums (Eqs. 5-7; g = 1 kernels instantiated with TRAJ)
   float* traj_s;
   float* traj_kbar;
@@ -798,6 +801,15 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
       ls = scol && !sel_sec ? sigma * (ck_sec + a_sec + qs * inv) : -INFINITY;
     }
 
+    if (TRACE && p.logit_n > 0 && t <= p.trace_steps) {
+      // SP_LOGITS: the step's whole logit vector after its record (token slots
+      // of masked tokens and past the group keep -inf), STOP last
+      float* lrec = p.trace + ((int64_t)g * p.trace_steps + (t - 1)) * p.trace_w + p.logit_off;
+      if (mcol) lrec[j] = selected ? -INFINITY : lj;
+      if (SEC && scol && sq == 0) lrec[js] = ls;
+      if (tid == 0) lrec[p.logit_n] = l_stop;
+    }
+
     if constexpr (GROUPED) {
       // ---- this wave's best gl candidates, descending (lowest index on ties)
       const int gl = gsz + (TRACE ? 1 : 0);
@@ -885,8 +897,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
       const unsigned long long stop_key = l_stop > -INFINITY ? cand_key(l_stop, n) : 0ull;
       const bool stop = top0 == 0ull || (!full && stop_key > top0);
       if (TRACE && tid == 0 && t <= p.trace_steps) {
-        const int tw = gsz + 3;
-        float* rec = p.trace + ((int64_t)g * p.trace_steps + (t - 1)) * tw;
+        float* rec = p.trace + ((int64_t)g * p.trace_steps + (t - 1)) * p.trace_w;
 #pragma unroll
         for (int r = 0; r < GMAX; ++r)
           if (r < gsz) rec[r] = __int_as_float(stop ? (r == 0 ? -1 : -3) : (r < cnt ? gi[r] : -3));
@@ -942,7 +953,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
           const float4 r = red[w];
           r2 = fmaxf(r2, __float_as_int(r.y) == a ? r.z : r.x);
         }
-        float* rec = p.trace + ((int64_t)g * p.trace_steps + (t - 1)) * 4;
+        float* rec = p.trace + ((int64_t)g * p.trace_steps + (t - 1)) * p.trace_w;
         rec[0] = __int_as_float(a == n ? -1 : a);
         rec[1] = kk ? key_value(kk) : l_stop;
         rec[2] = r2;
@@ -1017,13 +1028,15 @@ __global__ void fill_nan_kernel(float* x, int64_t count) {
   if (i < count) x[i] = __int_as_float(0x7fc00000);
 }
 
-// Trace records (width floats) past an episode's end carry taken = -2.
-__global__ void trace_fill_kernel(float* trace, int64_t count, int width) {
+// Trace records (width floats) past an episode's end carry taken = -2; the
+// logit vectors of SP_LOGITS (from float lo on) start at -inf.
+__global__ void trace_fill_kernel(float* trace, int64_t count, int width, int lo) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < count) {
     float* rec = trace + i * width;
     rec[0] = __int_as_float(-2);
-    for (int k = 1; k < width; ++k) rec[k] = 0.0f;
+    for (int k = 1; k < lo; ++k) rec[k] = 0.0f;
+    for (int k = lo; k < width; ++k) rec[k] = -INFINITY;
   }
 }
 
@@ -1154,10 +1167,13 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   if (gram_only) return hipGetLastError();
 
   const bool trace = (a.flags & SP_TRACE) && a.trace && a.trace_steps > 0;
+  const int rec_base = a.g > 1 ? a.g + 3 : 4;
+  const int logit_n = trace && (a.flags & SP_LOGITS) ? a.max_group : 0;
+  const int trace_w = rec_base + (logit_n > 0 ? logit_n + 1 : 0);
   if (trace) {
     const int64_t count = (int64_t)a.G * a.trace_steps;
     hipLaunchKernelGGL(trace_fill_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0,
-                       stream, a.trace, count, a.g > 1 ? a.g + 3 : 4);
+                       stream, a.trace, count, trace_w, rec_base);
   }
 
   SelParams p;
@@ -1180,6 +1196,9 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.grp_cnt_out = a.grp_cnt;
   p.trace = trace ? a.trace : nullptr;
   p.trace_steps = trace ? a.trace_steps : 0;
+  p.trace_w = trace_w;
+  p.logit_off = rec_base;
+  p.logit_n = logit_n;
   const bool traj = a.traj_s != nullptr;
   p.traj_s = a.traj_s;
   p.traj_kbar = a.traj_kbar;

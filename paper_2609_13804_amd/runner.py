@@ -36,14 +36,20 @@ class DeviceRun:
 
     def __init__(self, w: W.Workload, inputs: Dict[str, np.ndarray], layout: W.Layout,
                  b_stop: float, device="cuda", trace_steps: int = 0, flags: int = 0,
-                 caps: Optional[np.ndarray] = None, max_group: Optional[int] = None):
+                 caps: Optional[np.ndarray] = None, max_group: Optional[int] = None,
+                 logits: bool = False):
+        """trace_steps > 0 allocates the per-step trace (SP_TRACE); with
+        ``logits`` every record also holds the step's whole logit vector
+        (SP_LOGITS)."""
         self.w = w
         self.layout = layout
         self.b_stop = float(b_stop)
-        self.flags = flags | (sp.SP_TRACE if trace_steps > 0 else 0)
+        logits = logits and trace_steps > 0
+        self.flags = flags | (sp.SP_TRACE if trace_steps > 0 else 0) | (sp.SP_LOGITS if logits else 0)
         self.trace_steps = trace_steps
         self.g = w.g
-        self.trace_width = 4 if w.g == 1 else w.g + 3
+        self.trace_base = 4 if w.g == 1 else w.g + 3
+        self.trace_width = self.trace_base
         dev = torch.device(device)
         tdt = torch_dtype(w.dtype)
         up = lambda a, dt=tdt: torch.from_numpy(np.ascontiguousarray(a)).to(device=dev, dtype=dt)
@@ -76,6 +82,8 @@ class DeviceRun:
                                                   default=1))),
                            kept_total=int(kept_off[-1]))
         s = self.sizes
+        if logits:
+            self.trace_width = self.trace_base + s.max_group + 1
         self.dims = sp.dims(w.d, w.d_text, w.h, sp.SP_F32 if w.dtype == "f32" else sp.SP_BF16)
         if w.layout == "padded":
             self.layout_code = sp.SP_LAYOUT_PADDED
@@ -184,6 +192,11 @@ class DeviceRun:
         idx = self.kept_idx.cpu().numpy()
         off = self.kept_off_host
         return [idx[off[b]:off[b] + cnt[b]].tolist() for b in range(self.sizes.B)]
+
+    def trace_logits(self):
+        """SP_LOGITS: [G, trace_steps, max_group + 1] float32, every step's logit
+        of each token slot (-inf where masked or past the group) and STOP last."""
+        return self.trace[..., self.trace_base:].cpu().numpy()
 
     def trace_actions(self):
         """Per group: the taken candidates in order (-1 = STOP); with g > 1 per

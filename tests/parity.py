@@ -8,7 +8,9 @@ Tolerances (the bar every GPU parity test applies):
   * text context: per-row normwise relative error <= 1e-5 (float32 both sides);
   * logits: |l_gpu - l_oracle| <= tol * scale_t with tol = 1e-3 (bfloat16
     workloads) or 1e-5 (float32), scale_t the larger of the two top logits'
-    magnitudes and the root mean square of the step's finite logits;
+    magnitudes and the root mean square of the step's finite logits; with the
+    SP_LOGITS dump this holds for every candidate of every step (tokens and
+    STOP), and the masked tokens (-inf) must be exactly the selected ones;
   * selections: staged (the oracle runs on the GPU's own projected rows and
     context) and teacher-forced (the oracle replays the GPU's actions): every
     GPU action must equal the oracle's argmax, except at steps whose oracle
@@ -51,6 +53,7 @@ class SelectReport:
     steps: int = 0
     exempt_steps: int = 0
     max_logit_err: float = 0.0
+    logits_checked: int = 0            # logit values compared element by element (SP_LOGITS)
     free_running_equal: int = 0
     free_running_checked: int = 0
     divergences: List[str] = field(default_factory=list)
@@ -72,15 +75,37 @@ def _close(a: float, b: float, tol: float) -> bool:
     return abs(a - b) <= tol
 
 
+def check_logit_vector(got: np.ndarray, st, n: int, tol: float, scale: float, where: str) -> float:
+    """One step's dumped logit vector (SP_LOGITS: token slots, then STOP)
+    against the oracle's step record: the same tokens masked (-inf), slots past
+    the group -inf, and every finite logit and the STOP logit within
+    tol * scale.  Returns the largest error over the scale."""
+    got = np.asarray(got, np.float64)
+    tok, stop = got[:n], got[-1]
+    want = np.asarray(st.logits, np.float64)
+    assert np.array_equal(np.isneginf(tok), np.isneginf(want)), f"{where}: masked tokens differ"
+    assert np.isneginf(got[n:-1]).all(), f"{where}: slots past the group are not -inf"
+    fin = np.isfinite(want)
+    assert np.isfinite(tok[fin]).all(), f"{where}: non-finite logit"
+    err = float(np.abs(tok[fin] - want[fin]).max()) if fin.any() else 0.0
+    if np.isfinite(st.stop_logit):
+        err = max(err, abs(float(stop) - st.stop_logit))
+    else:
+        assert stop == st.stop_logit, f"{where}: STOP logit {stop!r} vs {st.stop_logit!r}"
+    assert err <= tol * scale, f"{where}: logit error {err:.3e} above {tol:g} x {scale:.3g}"
+    return err / scale
+
+
 def check_selection(KQV: np.ndarray, ctx: np.ndarray, grp_off, grp_img, caps, b_stop: float, h: int,
                     actions: Sequence[Sequence[int]], trace: Optional[np.ndarray], dtype: str,
                     no_history: bool = False, groups: Optional[Sequence[int]] = None,
-                    ignore_stop: bool = False) -> SelectReport:
+                    ignore_stop: bool = False, logits: Optional[np.ndarray] = None) -> SelectReport:
     """Staged, teacher-forced check of every episode in ``groups``.
 
     ``actions[g]`` is the GPU's taken-candidate sequence of group g (token index,
     -1 for STOP) and ``trace[g, t]`` its step record {taken, logit, runner-up,
-    STOP logit}.  Raises AssertionError on the first violation."""
+    STOP logit}; ``logits[g, t]`` (SP_LOGITS) the step's whole logit vector,
+    token slots then STOP.  Raises AssertionError on the first violation."""
     tol = logit_tol(dtype)
     rep = SelectReport()
     T_vis = KQV.shape[0] - 2
@@ -130,6 +155,10 @@ def check_selection(KQV: np.ndarray, ctx: np.ndarray, grp_off, grp_img, caps, b_
                 assert all(_close(x, y, tol * scale) for x, y in zip(pair_gpu, pair_or)), (
                     f"{where} step {t + 1}: top-2 {pair_gpu} vs {pair_or}")
                 rep.max_logit_err = max(rep.max_logit_err, err / scale)
+            if logits is not None:
+                e = check_logit_vector(logits[g, t], st, n, tol, scale, f"{where} step {t + 1}")
+                rep.max_logit_err = max(rep.max_logit_err, e)
+                rep.logits_checked += int(np.isfinite(st.logits).sum()) + 1
         if exempt_here == 0:
             free = oracle.run_episode(*args, no_history=no_history, keep_steps=False,
                                       ignore_stop=ignore_stop)
@@ -160,7 +189,8 @@ def kept_from_actions(actions, grp_off, grp_img, img_off, B):
 def check_grouped_selection(KQV: np.ndarray, ctx: np.ndarray, grp_off, grp_img, caps, b_stop: float,
                             h: int, gsize: int, rounds: Sequence[Sequence[Sequence[int]]],
                             trace: Optional[np.ndarray], dtype: str, no_history: bool = False,
-                            groups: Optional[Sequence[int]] = None) -> SelectReport:
+                            groups: Optional[Sequence[int]] = None,
+                            logits: Optional[np.ndarray] = None) -> SelectReport:
     """The staged, teacher-forced check with g = gsize tokens per round.
 
     ``rounds[g]`` is the GPU's round sequence of group g: per round the taken
@@ -225,6 +255,10 @@ def check_grouped_selection(KQV: np.ndarray, ctx: np.ndarray, grp_off, grp_img, 
                         f"{where} round {t + 1}: {what} logit {got!r} vs oracle {want!r} (scale {scale:.3g})")
                     if np.isfinite(want):
                         rep.max_logit_err = max(rep.max_logit_err, abs(got - want) / scale)
+            if logits is not None:
+                e = check_logit_vector(logits[g, t], st, n, tol, scale, f"{where} round {t + 1}")
+                rep.max_logit_err = max(rep.max_logit_err, e)
+                rep.logits_checked += int(np.isfinite(st.logits).sum()) + 1
         if exempt_here == 0:
             free = oracle.run_episode(*args, no_history=no_history, keep_steps=False, g=gsize)
             rep.free_running_checked += 1

@@ -3,13 +3,15 @@ tokens per round (Eq. 11), at full size, launched exactly as bench.py
 launches them (one stream, untraced selection kernel), checked against the
 oracle on outputs it can compute one by one:
 
-  * projection: a seeded sample of rows plus the START and STOP rows;
+  * projection: a seeded sample of rows plus the START and STOP rows (every
+    row is compared in tests/test_gpu_end_to_end.py);
   * text context: a sample of images;
-  * selection: every episode's count and kept set against the traced kernel's
-    own action sequence (which must take the same decisions as the untraced
-    kernel), and a sample of episodes (always including the longest and a
-    capped one) replayed teacher-forced and free-running in the oracle on the
-    GPU's projected rows (tests/parity.py protocol);
+  * selection: EVERY episode replayed in the oracle on the GPU's projected
+    rows (tests/parity.py protocol: staged, teacher-forced on the traced
+    kernel's actions, free-running when no step is a near-tie), with every
+    step's whole logit vector (SP_LOGITS) compared element by element; the
+    traced kernel must take the untraced (benchmarked) kernel's decisions,
+    and every count and kept set must equal the traced actions;
   * compaction: three feature columns of every output row for the whole batch,
     and every column of the rows of a sample of images, bit-exact.
 
@@ -29,36 +31,13 @@ from tests import parity
 pytestmark = pytest.mark.gpu
 
 SAMPLE_ROWS = 384
-SAMPLE_GROUPS = 16
 SAMPLE_IMAGES = 3
+CHUNK = 64          # episodes per progress line
 
 
 def _rounds(cap, n, g):
     """Rounds of an episode that never stops: the cap or ceil(n / g)."""
     return min(int(cap), -(-int(n) // g))
-
-
-def _sample_groups(rng, sizes, caps, steps, k, g):
-    """k groups: the longest episode, a capped one if any, the rest at random."""
-    G = len(sizes)
-    chosen = [int(np.argmax(steps))]
-    capped = [i for i in range(G) if steps[i] == _rounds(caps[i], sizes[i], g) and caps[i] > 0]
-    if capped:
-        chosen.append(int(capped[len(capped) // 2]))
-    rest = [i for i in range(G) if i not in chosen]
-    extra = rng.choice(rest, size=min(len(rest), max(0, k - len(chosen))), replace=False)
-    return sorted(set(chosen) | set(int(i) for i in extra))
-
-
-def _sub_episodes(KQV_dev, grp_off, groups, T_vis):
-    """Host float64 copy of the sampled groups' rows followed by the START and
-    STOP rows, with the group offsets into it."""
-    rows = np.concatenate([np.arange(grp_off[g], grp_off[g + 1]) for g in groups]
-                          + [np.array([T_vis, T_vis + 1])])
-    sub = KQV_dev[torch.from_numpy(rows).to(KQV_dev.device)].double().cpu().numpy()
-    sizes = [int(grp_off[g + 1] - grp_off[g]) for g in groups]
-    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
-    return sub, off
 
 
 @pytest.mark.parametrize("name", W.PAPER_WORKLOADS + W.GROUPED_WORKLOADS)
@@ -72,7 +51,7 @@ def test_full_size_parity(gpu_lib, name):
     steps_max = int(max(_rounds(c, n, w.g) for c, n in zip(lay.grp_cap, sizes))) + 1
     print(f"{name}: {lay.batch} images, {lay.groups} groups, {int(lay.img_off[-1])} tokens",
           flush=True)
-    run = DeviceRun(w, inp, lay, b_stop, trace_steps=steps_max)
+    run = DeviceRun(w, inp, lay, b_stop, trace_steps=steps_max, logits=True)
     rng = np.random.default_rng([2609, w.cfg_id])
 
     # ---- the benchmark's launch sequence
@@ -104,8 +83,9 @@ def test_full_size_parity(gpu_lib, name):
         c = oracle.text_context(inp["E_text"][t0:t1], np.array([0, t1 - t0]), inp["W_text"])
         assert parity.rows_relerr(ctx[b:b + 1], c) <= 1e-5, f"image {b}"
 
-    # ---- selection: the traced kernel decides as the benchmarked one did
-    run.select(flags=sp.SP_TRACE)
+    # ---- selection: the traced kernel (with the logit dump) decides as the
+    # benchmarked one did
+    run.select(flags=run.flags)
     torch.cuda.synchronize()
     assert run.device_errors() == [0, 0, 0]
     actions = run.trace_actions()
@@ -119,21 +99,35 @@ def test_full_size_parity(gpu_lib, name):
         assert (s and s[-1] == stop and len(s) <= r + 1) or len(s) == int(lay.grp_cap[g]), g
     steps = np.array([len(s) for s in actions])
 
-    groups = _sample_groups(rng, sizes, lay.grp_cap, steps, SAMPLE_GROUPS, w.g)
-    sub, sub_off = _sub_episodes(run.KQV, lay.grp_off, groups, T_vis)
-    trace = run.trace.cpu().numpy()[groups]
-    if w.g == 1:
-        rep = parity.check_selection(sub, ctx, sub_off, lay.grp_img[groups], lay.grp_cap[groups],
-                                     b_stop, w.h, [actions[g] for g in groups], trace, w.dtype)
-    else:
-        rep = parity.check_grouped_selection(sub, ctx, sub_off, lay.grp_img[groups],
-                                             lay.grp_cap[groups], b_stop, w.h, w.g,
-                                             [actions[g] for g in groups], trace, w.dtype)
-    print(f"{name}: checked {rep.episodes} of {lay.groups} episodes ({rep.steps} steps, longest "
-          f"{int(steps.max())}), {rep.exempt_steps} exempt, max logit err "
-          f"{rep.max_logit_err:.2e}, free-running equal {rep.free_running_equal}/"
-          f"{rep.free_running_checked}; kept total {sum(map(len, kept))}", flush=True)
-    del sub
+    # ---- every episode against the oracle, on the GPU's projected rows
+    KQV = run.KQV.float().cpu().numpy()          # exact: bf16 and f32 widen to f32
+    trace = run.trace.cpu().numpy()
+    logits = run.trace_logits()
+    total = parity.SelectReport()
+    for c0 in range(0, lay.groups, CHUNK):
+        chunk = range(c0, min(lay.groups, c0 + CHUNK))
+        if w.g == 1:
+            rep = parity.check_selection(KQV, ctx, lay.grp_off, lay.grp_img, lay.grp_cap, b_stop,
+                                         w.h, actions, trace, w.dtype, groups=chunk, logits=logits)
+        else:
+            rep = parity.check_grouped_selection(KQV, ctx, lay.grp_off, lay.grp_img, lay.grp_cap,
+                                                 b_stop, w.h, w.g, actions, trace, w.dtype,
+                                                 groups=chunk, logits=logits)
+        for f in ("episodes", "steps", "exempt_steps", "logits_checked", "free_running_equal",
+                  "free_running_checked"):
+            setattr(total, f, getattr(total, f) + getattr(rep, f))
+        total.max_logit_err = max(total.max_logit_err, rep.max_logit_err)
+        total.divergences += rep.divergences
+        print(f"{name}: episodes {c0}..{chunk[-1]} checked", flush=True)
+    assert total.episodes == lay.groups
+    print(f"{name}: checked {total.episodes} of {lay.groups} episodes ({total.steps} steps, longest "
+          f"{int(steps.max())}; {total.logits_checked} logits element by element), "
+          f"{total.exempt_steps} exempt, max logit err {total.max_logit_err:.2e}, free-running "
+          f"equal {total.free_running_equal}/{total.free_running_checked}; kept total "
+          f"{sum(map(len, kept))}", flush=True)
+    for d in total.divergences:
+        print(f"{name}: near-tie {d}", flush=True)
+    del KQV, trace, logits
 
     # ---- compaction
     if run.out is not None:

@@ -9,7 +9,9 @@ element by element against the oracle (tests/parity.py protocol):
 
 with caps that keep the history in registers, and caps that push it through
 the LDS rows and the re-read tier.  Each case runs the untraced kernel (the
-benchmark's) and the traced one, which must take the same decisions.
+benchmark's) and the traced one, which must take the same decisions; the
+traced run dumps every step's whole logit vector (SP_LOGITS), compared with
+the oracle's element by element.
 """
 import math
 
@@ -52,14 +54,14 @@ def test_group_shape(gpu_lib, name, cfg, tokens, cap, b_stop):
     inp = W.make_inputs(w)
     sizes = np.diff(lay.grp_off)
     steps = int(max(min(int(c), int(n)) for c, n in zip(lay.grp_cap, sizes))) + 1
-    run = DeviceRun(w, inp, lay, b_stop, trace_steps=steps)
+    run = DeviceRun(w, inp, lay, b_stop, trace_steps=steps, logits=True)
     run.project()
     run.select(flags=0)
     run.compact()
     torch.cuda.synchronize()
     assert run.device_errors() == [0, 0, 0]
     plain = run.kept_lists()
-    run.select(flags=sp.SP_TRACE)
+    run.select(flags=sp.SP_TRACE | sp.SP_LOGITS)
     torch.cuda.synchronize()
     assert run.device_errors() == [0, 0, 0]
     assert run.kept_lists() == plain
@@ -67,7 +69,8 @@ def test_group_shape(gpu_lib, name, cfg, tokens, cap, b_stop):
     KQV = run.KQV.double().cpu().numpy()
     ctx = run.ctx.double().cpu().numpy()
     rep = parity.check_selection(KQV, ctx, lay.grp_off, lay.grp_img, lay.grp_cap, b_stop, w.h,
-                                 actions, run.trace.cpu().numpy(), w.dtype)
+                                 actions, run.trace.cpu().numpy(), w.dtype,
+                                 logits=run.trace_logits())
     assert plain == parity.kept_from_actions(actions, lay.grp_off, lay.grp_img, lay.img_off,
                                              lay.batch)
     print(f"{name}: {rep.episodes} episodes, {rep.steps} steps, {rep.exempt_steps} exempt, "

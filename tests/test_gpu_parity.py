@@ -27,8 +27,14 @@ def _setup(name, b_stop=None, caps=None, flags=0, trace=True, images=None):
     b = W.stop_bias(w) if b_stop is None else b_stop
     c = lay.grp_cap if caps is None else np.asarray(caps, np.int32)
     steps = int(max(min(int(x), int(n)) for x, n in zip(c, np.diff(lay.grp_off)))) + 1 if trace else 0
-    run = DeviceRun(w, inp, lay, b, trace_steps=steps, flags=flags, caps=c)
+    run = DeviceRun(w, inp, lay, b, trace_steps=steps, flags=flags, caps=c, logits=trace)
     return w, inp, lay, run
+
+
+def _logits(run):
+    """The SP_LOGITS dump of a traced run (every step's whole logit vector)."""
+    from paper_2609_13804_amd import binding as sp
+    return run.trace_logits() if run.flags & sp.SP_LOGITS else None
 
 
 def _staged(run):
@@ -71,7 +77,7 @@ def test_selection_and_compaction_parity(gpu_lib, name):
     actions = run.trace_actions()
     tr = run.trace.cpu().numpy()
     rep = parity.check_selection(KQV, ctx, lay.grp_off, lay.grp_img, run.caps_host, run.b_stop,
-                                 w.h, actions, tr, w.dtype)
+                                 w.h, actions, tr, w.dtype, logits=_logits(run))
     print(f"{name}: {rep.episodes} episodes, {rep.steps} steps, {rep.exempt_steps} exempt, "
           f"max logit err {rep.max_logit_err:.2e}")
     kept = run.kept_lists()
@@ -154,7 +160,8 @@ def test_never_stop_is_identity(gpu_lib):
         assert np.array_equal(out[base:base + len(want)], want)
     KQV, ctx = _staged(run)
     parity.check_selection(KQV, ctx, lay.grp_off, lay.grp_img, caps, -math.inf, w.h,
-                           run.trace_actions(), run.trace.cpu().numpy(), w.dtype)
+                           run.trace_actions(), run.trace.cpu().numpy(), w.dtype,
+                           logits=_logits(run))
 
 
 def test_no_history_is_topk(gpu_lib):
@@ -168,7 +175,8 @@ def test_no_history_is_topk(gpu_lib):
     KQV, ctx = _staged(run)
     actions = run.trace_actions()
     parity.check_selection(KQV, ctx, lay.grp_off, lay.grp_img, run.caps_host, run.b_stop, w.h,
-                           actions, run.trace.cpu().numpy(), w.dtype, no_history=True)
+                           actions, run.trace.cpu().numpy(), w.dtype, no_history=True,
+                           logits=_logits(run))
     h = w.h
     T_vis = KQV.shape[0] - 2
     for g, seq in enumerate(actions):
@@ -203,7 +211,8 @@ def test_duplicate_rows_identical_logits(gpu_lib):
             assert lo in seq and seq.index(lo) < seq.index(hi)
     KQV, ctx = _staged(run)
     parity.check_selection(KQV, ctx, lay.grp_off, lay.grp_img, run.caps_host, -math.inf, w.h,
-                           run.trace_actions(), run.trace.cpu().numpy(), w.dtype)
+                           run.trace_actions(), run.trace.cpu().numpy(), w.dtype,
+                           logits=_logits(run))
 
 
 @pytest.mark.parametrize("name", ["mid_bf16", "mid_g5_bf16"])
@@ -300,7 +309,7 @@ def test_images_without_groups(gpu_lib):
     KQV, ctx = _staged(run)
     actions = run.trace_actions()
     parity.check_selection(KQV, ctx, lay.grp_off, lay.grp_img, run.caps_host, run.b_stop, w.h,
-                           actions, run.trace.cpu().numpy(), w.dtype)
+                           actions, run.trace.cpu().numpy(), w.dtype, logits=_logits(run))
     assert run.kept_lists() == parity.kept_from_actions(actions, lay.grp_off, lay.grp_img,
                                                         lay.img_off, lay.batch)
     w0 = W.Workload("no_groups", 110, batch=2, d=256, d_text=256, h=128, dtype="bf16",
@@ -397,7 +406,7 @@ def test_long_episodes_cross_every_history_tier(gpu_lib):
     assert [len(a) for a in actions] == [int(c) if c <= n else int(n) + 1
                                          for c, n in zip(caps, np.diff(lay.grp_off))]
     rep = parity.check_selection(KQV, ctx, lay.grp_off, lay.grp_img, caps, -math.inf, w.h,
-                                 actions, run.trace.cpu().numpy(), w.dtype)
+                                 actions, run.trace.cpu().numpy(), w.dtype, logits=_logits(run))
     print(f"long episodes: {rep.steps} steps, {rep.exempt_steps} exempt, "
           f"max logit err {rep.max_logit_err:.2e}")
 

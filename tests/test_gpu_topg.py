@@ -16,6 +16,7 @@ import pytest
 import torch
 
 import oracle
+from paper_2609_13804_amd import binding as sp
 from paper_2609_13804_amd import workloads as W
 from tests import parity
 
@@ -33,7 +34,7 @@ def _setup(w, b_stop=None, caps=None, flags=0, trace=True):
     b = W.stop_bias(w) if b_stop is None else b_stop
     c = lay.grp_cap if caps is None else np.asarray(caps, np.int32)
     steps = _rounds_bound(c, np.diff(lay.grp_off), w.g) if trace else 0
-    run = DeviceRun(w, inp, lay, b, trace_steps=steps, flags=flags, caps=c)
+    run = DeviceRun(w, inp, lay, b, trace_steps=steps, flags=flags, caps=c, logits=trace)
     return inp, lay, run
 
 
@@ -44,7 +45,9 @@ def _check(w, inp, lay, run, no_history=False, compact=True):
     rounds = run.trace_actions()
     rep = parity.check_grouped_selection(KQV, ctx, lay.grp_off, lay.grp_img, run.caps_host,
                                          run.b_stop, w.h, w.g, rounds, run.trace.cpu().numpy(),
-                                         w.dtype, no_history=no_history)
+                                         w.dtype, no_history=no_history,
+                                         logits=run.trace_logits() if run.flags & sp.SP_LOGITS
+                                         else None)
     kept = run.kept_lists()
     assert kept == parity.kept_from_actions(rounds, lay.grp_off, lay.grp_img, lay.img_off, lay.batch)
     assert run.grp_cnt.cpu().numpy()[:lay.groups].tolist() == [len(parity._flat(s)) for s in rounds]
@@ -82,7 +85,7 @@ def test_grouped_trace_and_plain_kernels_agree(gpu_lib, name):
     torch.cuda.synchronize()
     assert run.device_errors() == [0, 0, 0]
     plain = run.kept_lists()
-    run.select(flags=sp.SP_TRACE)
+    run.select(flags=run.flags)
     torch.cuda.synchronize()
     assert traced == plain == run.kept_lists()
 
@@ -148,7 +151,7 @@ def test_grouped_group_shapes(gpu_lib, name, cfg, tokens, cap, b_stop):
     torch.cuda.synchronize()
     assert run.device_errors() == [0, 0, 0]
     plain = run.kept_lists()
-    run.select(flags=sp.SP_TRACE)
+    run.select(flags=run.flags)
     run.compact()
     torch.cuda.synchronize()
     _, kept = _check(w, inp, lay, run)
