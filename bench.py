@@ -17,8 +17,10 @@ Two timed passes over K steps each, after W untimed warm-up steps:
   * pipelined (the reported "value", whole-job throughput): projections on one
     stream in batch order and each batch's select + compact on one of S select
     streams over a ring of buffer slots (runner.Pipeline), so that one batch's
-    projection and Gram products run beside earlier batches' recurrences; at
-    least 64 untimed batches fill and warm the pipeline first.
+    projection and Gram products run beside earlier batches' recurrences; each
+    slot holds its own seeded batch of the same shape (over 256 MB of tokens in
+    all on the default batch, more than the Infinity Cache holds); at least 64
+    untimed batches fill and warm the pipeline first.
 
 Prints one JSON line.  "roofline" covers the kernel with the largest share of
 the GPU (kernel time x fraction of the compute units it occupies), with its HBM
@@ -46,9 +48,12 @@ PEAK_F32_MATRIX_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 # float32 FMA without packed instructions: 256 CU x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz
 PEAK_F32_VALU_TFLOPS = 78.6
-# LDS reads: 256 B/clk per CU measured on gfx950 with the GEMM's ds_read_b128
-# pattern, x 256 CUs x 2.4 GHz
+# LDS reads: 256 B/clk per CU x 256 CUs x 2.4 GHz, the rate the LDS probe
+# (csrc/probe.hip, bench.py --lds-probe) measures on gfx950 with 16-byte reads;
+# every run also reports its own probe measurement in measured_peaks
 PEAK_LDS_GBS = 157286.0
+NOMINAL_CLOCK_HZ = 2.4e9
+N_CU = 256
 
 # minimum untimed warm-up of the pipelined pass, in batches (about 25 ms of
 # overlapped work on the 16-image batch)
@@ -304,11 +309,48 @@ def measured_peaks():
         rates[f"{mm}x{kk}x{nn}"] = round(2.0 * mm * kk * nn * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e12, 1)
         del a, b, c
     torch.cuda.empty_cache()
+    res.update(lds_probe())
     res["bf16_matmul_TFLOPs"] = max(rates.values())
     res["bf16_matmul_by_shape"] = rates
     res["how"] = ("1 GiB device copy (read + write bytes); the best torch bf16 matmul rate "
-                  "(M x K x N) of the shapes listed; 10 launches each after 3 warm-up")
+                  "(M x K x N) of the shapes listed; the LDS read probe; 10 launches each "
+                  "after 3 warm-up")
     return res
+
+
+def lds_probe(launches=10, warmup=3, iters=2048):
+    """LDS read bandwidth of the whole chip: the probe kernel of
+    libstepprune_probe.so (16-byte reads, two 512-thread workgroups per
+    compute unit, 64 KB of LDS each), timed with events on torch's current
+    stream, where it is launched."""
+    import torch
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_13804_amd", "libstepprune_probe.so"))
+    lib.stepprune_probe_lds.restype = ctypes.c_int
+    lib.stepprune_probe_lds.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                                        ctypes.c_void_p]
+    threads = int(lib.stepprune_probe_lds_threads())
+    blocks = 8 * N_CU
+    out = torch.empty(blocks * threads, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def launch():
+        if lib.stepprune_probe_lds(out.data_ptr(), blocks, iters, stream) != 0:
+            raise RuntimeError("LDS probe launch failed")
+    for _ in range(warmup):
+        launch()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(launches):
+        launch()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / launches
+    nbytes = blocks * threads * iters * 8 * 16
+    gbs = nbytes / (us * 1e-6) / 1e9
+    return {"lds_read_GBs": round(gbs, 1), "lds_probe_us": round(us, 2),
+            "lds_read_B_per_clk_per_cu_at_2.4GHz": round(gbs * 1e9 / (N_CU * NOMINAL_CLOCK_HZ), 1),
+            "lds_probe": f"{blocks} workgroups x {threads} threads x {iters} rounds of 8 "
+                         f"16-byte reads ({nbytes / 1e9:.1f} GB a launch)"}
 
 
 def copy_probe(mib):
@@ -426,6 +468,11 @@ def main(argv=None):
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (5 launches), the "
                          "calibration for the FETCH_SIZE / WRITE_SIZE counters, and exit")
+    ap.add_argument("--lds-probe", action="store_true",
+                    help="only run the LDS read probe (10 timed launches), print its rate and exit")
+    ap.add_argument("--shared-inputs", action="store_true",
+                    help="pipelined pass: every slot reads the first batch's tokens (by default "
+                         "each slot has its own seeded batch, so tokens come from HBM)")
     args = ap.parse_args(argv)
     if args.hw_queues:
         if not 1 <= args.hw_queues <= 32:
@@ -434,6 +481,10 @@ def main(argv=None):
         os.environ["GPU_MAX_HW_QUEUES"] = str(args.hw_queues)   # read when HIP starts
     if args.copy_probe_mib:
         return copy_probe(args.copy_probe_mib)
+    if args.lds_probe:
+        _ensure_built()
+        print(json.dumps(lds_probe()), flush=True)
+        return 0
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU only: the selection path shards by image with no "
@@ -583,7 +634,11 @@ def main(argv=None):
                    "frac_keyscan_roofline": round(t_scan_roof / (stages["select"] * 1e-6), 4),
                    "keyscan_roofline_us": round(t_scan_roof * 1e6, 2)},
         "compact": {"bound": "hbm", "frac": frac(work["compact_gather"][1], PEAK_HBM_GBS,
-                                                 stages["compact"])},
+                                                 stages["compact"]),
+                    "frac_kernel": frac(work["compact_gather"][1], PEAK_HBM_GBS,
+                                        kernels["compact_gather"]),
+                    "kernel_us": round(kernels["compact_gather"], 2),
+                    "algorithmic": f"{work['compact_gather'][1]:.6g} GB per launch"},
     }
 
     # Pipelined pass: projections on one stream in batch order, batch k's
@@ -592,15 +647,22 @@ def main(argv=None):
     # earlier batches' recurrences (one workgroup per episode) leave free.
     # --schedule rr instead issues whole batches round-robin on S streams.
     S = max(1, args.streams)
+    slot_inputs = None
     if S > 1:
         from paper_2609_13804_amd.runner import Pipeline
+        n_slots = max(S, args.slots) if args.schedule.startswith("staggered") else S
+        if not args.shared_inputs:
+            # a stream of fresh batches: every slot its own seeded tokens (same
+            # sizes), so no batch's tokens are still in the caches from the last
+            slot_inputs = [W.make_inputs(w, batch_index=k) for k in range(1, n_slots)]
         if args.schedule.startswith("staggered"):
-            pipe = Pipeline(run, max(S, args.slots), min(S, Pipeline.max_streams()),
-                            split_gram=args.schedule == "staggered-gram")
+            pipe = Pipeline(run, n_slots, min(S, Pipeline.max_streams()),
+                            split_gram=args.schedule == "staggered-gram", inputs=slot_inputs)
             runs = pipe.runs
             issue = lambda k: pipe.issue()
         else:
-            runs = [run] + [run.sibling() for _ in range(S - 1)]
+            runs = [run] + [run.sibling(None if slot_inputs is None else slot_inputs[k])
+                            for k in range(S - 1)]
             streams = [torch.cuda.Stream() for _ in range(S)]     # default priority
             def issue(k):
                 r, st = runs[k % S], streams[k % S].cuda_stream
@@ -608,6 +670,13 @@ def main(argv=None):
                 r.select(st)
                 if r.out is not None:
                     r.compact(st)
+        # Each slot's own result, one stream at a time, for the check below.
+        slot_inputs = None
+        refs = []
+        for r in runs:
+            r.run()
+            torch.cuda.synchronize()
+            refs.append((r.kept_idx.clone(), None if r.out is None else r.out.clone()))
         # Untimed warm-up of the overlapped streams: at least W batches, every
         # slot used, and at least PIPE_WARMUP_BATCHES in all.  In a fresh process
         # the first few tens of milliseconds of overlapped work have run up to
@@ -623,10 +692,11 @@ def main(argv=None):
         errs = [e for r in runs for e in r.device_errors()]
         if any(errs):
             raise RuntimeError(f"device error words {errs}")
-        for r in runs[1:]:
-            if not (torch.equal(r.kept_idx, run.kept_idx) and
-                    (r.out is None or torch.equal(r.out, run.out))):
-                raise RuntimeError("streams disagree on the same batch")
+        for r, (kept_ref, out_ref) in zip(runs, refs):
+            if not (torch.equal(r.kept_idx, kept_ref) and
+                    (r.out is None or torch.equal(r.out, out_ref))):
+                raise RuntimeError("the overlapped streams disagree with one stream on a batch")
+        del refs
         elapsed = t1 - t0
     value = K * s.B / elapsed
 
@@ -641,6 +711,11 @@ def main(argv=None):
             gram_flop, mpeak["mfma"], kernels["gram_gemm"])
     stage_roofline["compact"]["frac_measured_peak"] = frac(
         work["compact_gather"][1], mpeak["hbm"], stages["compact"])
+    stage_roofline["compact"]["frac_kernel_measured_peak"] = frac(
+        work["compact_gather"][1], mpeak["hbm"], kernels["compact_gather"])
+    t_scan_meas = max(lds_scan / (peaks["lds_read_GBs"] * 1e9), hbm_keys / (PEAK_HBM_GBS * 1e9))
+    stage_roofline["select"]["frac_keyscan_roofline_measured_lds"] = round(
+        t_scan_meas / (stages["select"] * 1e-6), 4)
     if mpeak.get(roofline["bound"]):
         roofline["measured_peak"] = mpeak[roofline["bound"]]
         roofline["frac_measured_peak"] = round(roofline["achieved"] / mpeak[roofline["bound"]], 4)
@@ -660,6 +735,8 @@ def main(argv=None):
         "data": "synthetic",
         "config": {"workload": w.name, "images": s.B, "groups": s.G, "streams": S,
                    "schedule": args.schedule if S > 1 else "single",
+                   "slot_inputs": ("shared" if args.shared_inputs else "own seeded batch per slot")
+                                  if S > 1 else None,
                    "slots": max(S, args.slots) if S > 1 and args.schedule != "rr" else S,
                    "tokens": int(s.T_vis), "d": w.d, "h": w.h, "text_tokens": int(s.T_txt),
                    "layout": w.layout, "b_stop": b_stop, "tokens_per_round": w.g,

@@ -1,4 +1,5 @@
-"""Build libstepprune.so for gfx950 with hipcc (in-tree, next to this file).
+"""Build libstepprune.so (and the benchmark's LDS probe, libstepprune_probe.so)
+for gfx950 with hipcc (in-tree, next to this file).
 
     python -m paper_2609_13804_amd.build [--jobs N] [--verbose]
 """
@@ -14,6 +15,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libstepprune.so")
+PROBE_LIB = os.path.join(HERE, "libstepprune_probe.so")
+PROBE_SOURCE = "probe.hip"
 BUILD_DIR = os.path.join(ROOT, "_build")
 
 SOURCES = ["api.hip", "gemm.hip", "select.hip", "text.hip", "compact.hip", "denoise.hip"]
@@ -21,6 +24,8 @@ SOURCES = ["api.hip", "gemm.hip", "select.hip", "text.hip", "compact.hip", "deno
 # alloca promotion use the whole VGPR budget instead of a quarter of it.
 EXTRA_FLAGS = {"select.hip": ["-mllvm", "-amdgpu-promote-alloca-to-vector-vgpr-ratio=1"]}
 ARCH = "gfx950"
+# roctx ranges around the entry points (rocprofiler-sdk's marker library)
+LINK_LIBS = ["-lrocprofiler-sdk-roctx"]
 # Packed fp32 ALU ops are disabled for every translation unit.
 HIPCC_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
                "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -60,8 +65,13 @@ def build(jobs: int = 8, verbose: bool = False) -> str:
     with concurrent.futures.ThreadPoolExecutor(max_workers=max(1, jobs)) as ex:
         list(ex.map(lambda c: _run(c, verbose), cmds))
     tmp = LIB + ".tmp"
-    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
+    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs, *LINK_LIBS],
+         verbose)
     os.replace(tmp, LIB)
+    # the benchmark's LDS bandwidth probe, a library of its own
+    tmp = PROBE_LIB + ".tmp"
+    _run([hipcc, *HIPCC_FLAGS, "-shared", "-o", tmp, os.path.join(CSRC, PROBE_SOURCE)], verbose)
+    os.replace(tmp, PROBE_LIB)
     return LIB
 
 

@@ -5,11 +5,22 @@
 
 #include <mutex>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "sp_internal.h"
 
 using namespace sp;
 
 namespace {
+
+// A roctx range named after the entry point around each call (host-side
+// enqueue), so a marker trace shows the three stages of Algorithm 1.
+struct TraceRange {
+  explicit TraceRange(const char* name) { roctxRangePushA(name); }
+  ~TraceRange() { roctxRangePop(); }
+  TraceRange(const TraceRange&) = delete;
+  TraceRange& operator=(const TraceRange&) = delete;
+};
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -111,6 +122,7 @@ sp_status stepprune_project(const sp_dims* dims, const void* X, int64_t T_vis, c
                             const int32_t* text_off, int32_t B, int64_t T_txt, const void* W_text,
                             float g_text, float ln_eps, void* KQV, float* ctx, void* ws,
                             size_t ws_bytes, const hipEvent_t* events, hipStream_t stream) {
+  const TraceRange range("stepprune_project");
   sp_status st = check_dims(dims);
   if (st != SP_OK) return st;
   if (T_vis < 0 || T_txt < 0 || B < 1) return SP_EINVAL;
@@ -273,6 +285,7 @@ sp_status stepprune_select(const sp_dims* dims, const void* KQV, const float* ct
                            int32_t* kept_cnt, int32_t* grp_cnt, float* trace, int32_t trace_steps,
                            void* ws, size_t ws_bytes, const hipEvent_t* events,
                            hipStream_t stream) {
+  const TraceRange range("stepprune_select");
   return select_impl(dims, KQV, ctx, T_vis, img_off, B, grp_off, grp_img, grp_cap, G, max_group,
                      max_cap, kept_off, b_stop, g, flags, kept_idx, kept_cnt, grp_cnt, trace,
                      trace_steps, nullptr, ws, ws_bytes, events, stream);
@@ -288,6 +301,7 @@ sp_status stepprune_select_trajectory(const sp_dims* dims, const void* KQV, cons
                                       int32_t trace_steps, const sp_trajectory* traj, void* ws,
                                       size_t ws_bytes, const hipEvent_t* events,
                                       hipStream_t stream) {
+  const TraceRange range("stepprune_select_trajectory");
   if (!traj) return SP_EINVAL;
   return select_impl(dims, KQV, ctx, T_vis, img_off, B, grp_off, grp_img, grp_cap, G, max_group,
                      max_cap, kept_off, b_stop, g, flags, kept_idx, kept_cnt, grp_cnt, trace,
@@ -303,6 +317,7 @@ sp_status stepprune_select_noalloc(const sp_dims* dims, const void* KQV, const f
                                    int32_t* kept_cnt, int32_t* grp_cnt, float* trace,
                                    int32_t trace_steps, int32_t* err,
                                    const hipEvent_t* events, hipStream_t stream) {
+  const TraceRange range("stepprune_select_noalloc");
   return select_impl(dims, KQV, ctx, T_vis, img_off, B, grp_off, grp_img, grp_cap, G, max_group,
                      max_cap, kept_off, b_stop, g, flags, kept_idx, kept_cnt, grp_cnt, trace,
                      trace_steps, nullptr, nullptr, 0, events, stream, true, err);
@@ -314,6 +329,7 @@ sp_status stepprune_compact(const sp_dims* dims, const void* X, const int32_t* i
                             int32_t layout, int32_t rows_per_image, int64_t out_rows, void* out,
                             int32_t* seq_info, void* ws, size_t ws_bytes,
                             const hipEvent_t* events, hipStream_t stream) {
+  const TraceRange range("stepprune_compact");
   sp_status st = check_dims(dims);
   if (st != SP_OK) return st;
   if (dims->d_text != dims->d) return SP_EUNSUPPORTED;
@@ -367,6 +383,7 @@ sp_status stepprune_gate_denoise(const sp_dims* dims, const void* X, int64_t T,
                                  const float* alpha, const void* eps, const sp_denoiser* p,
                                  void* out, void* ws, size_t ws_bytes,
                                  const hipEvent_t* events, hipStream_t stream) {
+  const TraceRange range("stepprune_gate_denoise");
   sp_status st = check_dims(dims);
   if (st != SP_OK) return st;
   if (dims->dtype != SP_BF16 || dims->d > 4096) return SP_EUNSUPPORTED;

@@ -117,10 +117,20 @@ class DeviceRun:
                     if w.d_text == w.d else None)
         self.ws = [torch.zeros(n, dtype=torch.uint8, device=dev) for n in self.ws_bytes]
 
-    def sibling(self):
-        """Another run of the same batch that shares the inputs (read only) and has
-        outputs and workspaces of its own, for work on a second stream."""
+    def sibling(self, inputs: Optional[Dict[str, np.ndarray]] = None):
+        """Another run with outputs and workspaces of its own, for work on a
+        second stream.  It shares the weights and offsets (read only), and the
+        visual and text tokens too unless ``inputs`` gives a batch of the same
+        shape (X and E_text are then uploaded for it)."""
         other = copy.copy(self)
+        if inputs is not None:
+            up = lambda a, ref: torch.from_numpy(np.ascontiguousarray(a)).to(device=ref.device,
+                                                                             dtype=ref.dtype)
+            if inputs["X"].shape != tuple(self.X.shape) or \
+                    inputs["E_text"].shape != tuple(self.E.shape):
+                raise ValueError("a sibling's batch must have the same shape")
+            other.X = up(inputs["X"], self.X)
+            other.E = up(inputs["E_text"], self.E)
         other._alloc_outputs()
         return other
 
@@ -231,7 +241,8 @@ class Pipeline:
     (SP_REUSE_GRAM) runs on the select stream; measured on the 16 x 576 batch
     this is slower (38K against 44K images/s): concurrent GEMMs of two
     batches fill each other's last tile rounds.  Batch k uses buffer slot k mod ``slots``, a
-    DeviceRun with its own outputs and workspaces (inputs shared read-only):
+    DeviceRun with its own outputs and workspaces (and its own tokens when
+    ``inputs`` are given; the weights are shared read-only):
     a slot's projection waits for the slot's previous select + compact, and
     its recurrence waits for its projection and Gram products.  More slots
     than select streams let the GEMM stream run ahead.  All streams use the
@@ -249,12 +260,19 @@ class Pipeline:
         default of four queues gives three)."""
         return max(1, int(os.environ.get("GPU_MAX_HW_QUEUES", "4")) - 1)
 
-    def __init__(self, run: DeviceRun, slots: int = 4, streams: int = 3, split_gram: bool = False):
+    def __init__(self, run: DeviceRun, slots: int = 4, streams: int = 3, split_gram: bool = False,
+                 inputs=None):
+        """``inputs``: None (every slot reads ``run``'s tokens) or one input
+        dict per further slot (slots - 1 of them), so that the stream of
+        batches reads fresh tokens from HBM rather than cached ones."""
         if not 1 <= streams <= self.max_streams():
             raise ValueError(f"streams must be 1..{self.max_streams()}")
         if slots < streams:
             raise ValueError("need at least one slot per select stream")
-        self.runs = [run] + [run.sibling() for _ in range(slots - 1)]
+        if inputs is not None and len(inputs) != slots - 1:
+            raise ValueError("one input batch per further slot")
+        self.runs = [run] + [run.sibling(None if inputs is None else inputs[k])
+                             for k in range(slots - 1)]
         self.proj_stream = torch.cuda.current_stream()
         self.sel_streams = [torch.cuda.Stream() for _ in range(streams)]
         self.projected = [torch.cuda.Event() for _ in self.runs]

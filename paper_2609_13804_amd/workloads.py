@@ -280,14 +280,19 @@ def make_text(w: Workload, index: int) -> np.ndarray:
     return _to_dtype_values(rng.standard_normal((w.text_len, w.d_text), dtype=np.float32), w.dtype)
 
 
-def make_inputs(w: Workload, images: Optional[List[int]] = None) -> Dict[str, np.ndarray]:
+def make_inputs(w: Workload, images: Optional[List[int]] = None,
+                batch_index: int = 0) -> Dict[str, np.ndarray]:
     """All inputs of a workload as float32 arrays holding dtype-exact values.
 
-    ``images`` restricts the batch to a subset (same per-image content)."""
+    ``images`` restricts the batch to a subset (same per-image content).
+    ``batch_index`` k > 0 draws the k-th further batch of a stream of batches:
+    the same image sizes (so the same layout) with fresh content, image i
+    drawn as image k * batch + i of the workload's streams."""
     sizes = image_sizes(w)
     idx = list(range(w.batch)) if images is None else list(images)
-    X = np.concatenate([make_image(w, i, sizes[i]) for i in idx], axis=0)
-    E = np.concatenate([make_text(w, i) for i in idx], axis=0)
+    base = batch_index * w.batch
+    X = np.concatenate([make_image(w, base + i, sizes[i]) for i in idx], axis=0)
+    E = np.concatenate([make_text(w, base + i) for i in idx], axis=0)
     out = make_weights(w)
     out.update(X=X, E_text=E)
     return out
