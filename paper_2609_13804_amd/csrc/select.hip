@@ -73,13 +73,16 @@ struct SelParams {
 //   hmain [64 W][lt]        lane-owned history past the registers (column-major)
 //   hsec  [ks / 16][64][4][4]  history of the second columns: entry 16 k + 4 q + e of
 //                           column 512 + c at [k][c][q][e] (quarter q of each block)
-//   alpha [alpha_ld]        softmax weights (unnormalised), written by wave 0; zero
-//                           past the current history
-//   sm    [4]               1 / softmax sum, STOP term of the older entries, newest weight
+//   alpha [copies][alpha_ld] softmax weights (unnormalised), zero past the current
+//                           history: g = 1, one copy per wave, written and read by
+//                           that wave alone; grouped rounds, one copy written by
+//                           wave 0
+//   sm    [4]               grouped rounds: 1 / softmax sum, STOP term of the older
+//                           entries
 //   hcol  [hcap]            history columns (START = n + 1)
 //   shist [hcap]            STOP column of the history B rows
-//   key   [2]               decision keys by step parity
-//   red   [16]              per-wave best and runner-up (tracing)
+//   key   [2][16]           g = 1: each wave's decision key, by step parity
+//   red   [2][16]           per-wave best and runner-up (tracing), by step parity
 //   cnt   [16]              end-of-episode counts
 //   ckeys [16][kGMax + 1]   grouped rounds: each wave's best keys, descending (slots
 //                           a launch never writes stay zero)
@@ -87,16 +90,16 @@ struct SelParams {
 //   zpart [2][16]           trajectory sums: per-wave partial softmax sums by step parity
 struct SelLds {
   int hmain, hsec, alpha, sm, hcol, shist, key, red, cnt, ckeys, ranked, zpart, total;
-  __host__ __device__ SelLds(int W, int lt, int ks, int alpha_ld, int hcap) {
+  __host__ __device__ SelLds(int W, int lt, int ks, int alpha_ld, int hcap, int copies) {
     hmain = 0;
     hsec = hmain + 64 * W * lt * 4;
     alpha = hsec + ks * 64 * 4;
-    sm = alpha + alpha_ld * 4;
+    sm = alpha + copies * alpha_ld * 4;
     hcol = sm + 16;
     shist = (hcol + hcap * 4 + 15) & ~15;
     key = (shist + hcap * 4 + 15) & ~15;
-    red = key + 16;
-    cnt = red + 16 * 16;
+    red = key + 2 * 16 * 8;
+    cnt = red + 2 * 16 * 16;
     ckeys = cnt + 16 * 4;
     ranked = ckeys + 16 * (kGMax + 1) * 8;
     zpart = ranked + 16 * (kGMax + 1) * 8;
@@ -247,10 +250,12 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   const bool no_history = (p.flags & SP_NO_HISTORY) != 0;
   const bool full = (p.flags & SP_FULL_ROLLOUT) != 0;   // STOP scored, never taken while tokens remain
   const int lt = p.lt, ks = p.ks;
-  const SelLds L(W, lt, ks, p.alpha_ld, p.hcap);
+  const SelLds L(W, lt, ks, p.alpha_ld, p.hcap, GROUPED ? 1 : W);
   float* hmain = reinterpret_cast<float*>(smem + L.hmain);
   float* hsec = reinterpret_cast<float*>(smem + L.hsec);
   float* alpha = reinterpret_cast<float*>(smem + L.alpha);
+  // this wave's copy of the history weights (g = 1), the shared one otherwise
+  float* alphaw = alpha + (GROUPED ? 0 : wave * p.alpha_ld);
   float* sm = reinterpret_cast<float*>(smem + L.sm);
   int* hcol = reinterpret_cast<int*>(smem + L.hcol);
   float* shist = reinterpret_cast<float*>(smem + L.shist);
@@ -272,6 +277,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   const int js = 512 + scl;
   const bool swave = SEC && wave < 4;
   const bool scol = swave && js < n;
+  const int jc = mcol ? j : 0, jsc = scol ? js : 0;   // columns a lane reads (0 when it has none)
   const float sigma = p.sigma, c1 = p.c1;
 
   auto ckv = [&](int c) { return (CK[c] + CK[ld + c]) + CK[2 * ld + c]; };
@@ -283,11 +289,10 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   if (SEC)
     for (int i = tid; i < ks * 16; i += 64 * W)
       reinterpret_cast<float4*>(hsec)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-  // alpha past the history stays zero: wave 0 (its only writer) clears it
-  // before its first softmax.
-  if (wave == 0)
-    for (int i = lane; i < p.alpha_ld; i += 64) alpha[i] = 0.0f;
-  if (tid < 2) key[tid] = 0ull;
+  // the weights past the history stay zero: each copy's only writer clears it
+  // before its first softmax
+  if (!GROUPED || wave == 0)
+    for (int i = lane; i < p.alpha_ld; i += 64) alphaw[i] = 0.0f;
   if (GROUPED)
     for (int i = tid; i < 16 * (kGMax + 1); i += 64 * W) ckeys[i] = 0ull;
 
@@ -306,16 +311,31 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   auto hput = [&](int pos, float x) {
     const int e = __builtin_amdgcn_readfirstlane(pos & 31);   // uniform: one indexed move
     const int k = __builtin_amdgcn_readfirstlane(pos >> 5);
-    if (__builtin_amdgcn_readfirstlane(k == 0)) h0[e] = x;
-    if (NV > 1 && __builtin_amdgcn_readfirstlane(k == 1)) h1[e] = x;
-    if (NV > 2 && __builtin_amdgcn_readfirstlane(k == 2)) h2[e] = x;
-    if (NV > 3 && __builtin_amdgcn_readfirstlane(k == 3)) h3[e] = x;
-    if (NV > 4 && __builtin_amdgcn_readfirstlane(k == 4)) h4[e] = x;
+    // one opaque scalar copy of k per test: scalar compares and branches
+    int k0 = k, k1 = k, k2 = k, k3 = k, k4 = k;
+    asm volatile("" : "+s"(k0), "+s"(k1), "+s"(k2), "+s"(k3), "+s"(k4));
+    if (k0 == 0) h0[e] = x;
+    if (NV > 1 && k1 == 1) h1[e] = x;
+    if (NV > 2 && k2 == 2) h2[e] = x;
+    if (NV > 3 && k3 == 3) h3[e] = x;
+    if (NV > 4 && k4 == 4) h4[e] = x;
+  };
+  // Slot pos of a four-register, 256-entry history array (entry lane + 64 k
+  // in register k): the owning lane takes v.  The register is chosen with a
+  // scalar comparison, the lane with a select.
+  auto put4 = [&](auto& r0, auto& r1, auto& r2, auto& r3, int pos, auto v) {
+    const int k = __builtin_amdgcn_readfirstlane(pos >> 6);
+    const bool mine = lane == (pos & 63);
+    r0 = mine && k == 0 ? v : r0;
+    r1 = mine && k == 1 ? v : r1;
+    r2 = mine && k == 2 ? v : r2;
+    r3 = mine && k == 3 ? v : r3;
   };
   // History column of entry lane + 64 k, for the first 256 entries.
   int hc0 = 0, hc1 = 0, hc2 = 0, hc3 = 0;
-  // Wave 0: the STOP column of the history's B rows, entry lane + 64 k in
-  // slot k (also kept in LDS for histories past 256 entries).
+  // The STOP column of the history's B rows, entry lane + 64 k in slot k (also
+  // kept in LDS for histories past 256 entries): every wave keeps it for
+  // g = 1, wave 0 for grouped rounds.
   float sh0 = 0.0f, sh1 = 0.0f, sh2 = 0.0f, sh3 = 0.0f;
 
   // The newest history entry (position hl - 1): its column, its A values, and
@@ -324,6 +344,9 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   float a_main = 0.0f, a_sec = 0.0f, a_stop = 0.0f;
   float b_main = 0.0f, b_sec = 0.0f, b_stop = 0.0f;
   int hl = 0;
+  // g = 1: this wave's softmax of the newest entry: the reciprocal of the
+  // weights' sum, the STOP term of the older entries and the newest weight.
+  float s_inv = 0.0f, s_st = 0.0f, s_enew = 0.0f;
   // Grouped rounds: the newest group (ng entries at the end of the history),
   // its rows, and its B values, stored into the history at the next decision.
   const int gsz = GROUPED ? p.g : 1;
@@ -336,21 +359,20 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     bg[i] = bgs[i] = bst[i] = 0.0f;
   }
 
-  // History softmax of the newest entry e (row r): unnormalised weights
-  // e_tau = exp(sigma (A[e, tau] - max)) into alpha, and into sm the reciprocal
-  // of their sum, the STOP term of the older entries (sum e_tau B[tau, STOP])
-  // and the newest entry's own weight.  Wave 0 only; the scores are gathered
-  // straight from the A row in the Gram buffer.
-  auto softmax_w0 = [&](const float* Ar) {
+  // g = 1: history softmax of the newest entry e (its A row Ar), run by every
+  // wave into its own weights: e_tau = exp(sigma (A[e, col(tau)] - max)), the
+  // reciprocal of their sum, the STOP term of the older entries (sum e_tau
+  // B[tau, STOP]) and the newest entry's own weight.  r0..r3 are the scores
+  // gathered at the history columns before the newest entry's column was set
+  // (its slot takes r_new, its own score); bst_prev is the STOP value of the
+  // entry stored into the history this step.
+  auto softmax_all = [&](const float* Ar, float r0, float r1, float r2, float r3, float r_new,
+                         float bst_prev) {
     const int hpad = (hl + 15) & ~15;
+    const int pos = hl - 1;
     float m, sum = 0.0f, s2 = 0.0f;
-    // The newest entry's own score, requested with the gathers below.
-    const float r_new = Ar[ecol];
     if (hl <= 256) {
-      // Every lane requests all four scores at once (columns without an entry
-      // hold a valid column), so the gathers share one memory round trip.
-      float r0 = Ar[hc0], r1 = Ar[hc1], r2 = Ar[hc2], r3 = Ar[hc3];
-      asm volatile("" : "+v"(r0), "+v"(r1), "+v"(r2), "+v"(r3));   // not sunk into branches
+      put4(r0, r1, r2, r3, pos, r_new);
       const float x0 = lane < hl ? r0 * c1 : -INFINITY;
       const float x1 = lane + 64 < hl ? r1 * c1 : -INFINITY;
       const float x2 = lane + 128 < hl ? r2 * c1 : -INFINITY;
@@ -361,61 +383,36 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
         const float e = tau < hl ? __builtin_amdgcn_exp2f(x - m) : 0.0f;
         sum += e;
         s2 = fmaf(e, tau < hl - 1 ? sh : 0.0f, s2);
-        if (tau < hpad) alpha[opaque(tau)] = e;
+        if (tau < hpad) alphaw[opaque(tau)] = e;
       };
       one(0, x0, sh0);
       if (64 < hpad) one(1, x1, sh1);
       if (128 < hpad) one(2, x2, sh2);
       if (192 < hpad) one(3, x3, sh3);
     } else {
-      // longer histories: the scores are gathered again in each pass
+      // longer histories: the scores are gathered again in each pass; the
+      // newest column and the STOP value stored this step come from registers
+      // (other waves' writes of this step need not be visible yet)
+      auto col = [&](int tau) { return tau == pos ? ecol : hcol[tau]; };
       m = -INFINITY;
-      for (int tau = lane; tau < hl; tau += 64) m = fmaxf(m, Ar[hcol[tau]] * c1);
+      for (int tau = lane; tau < hl; tau += 64) m = fmaxf(m, Ar[col(tau)] * c1);
       m = wave_max_fused(m);
       for (int tau = lane; tau < hpad; tau += 64) {
-        const float e = tau < hl ? __builtin_amdgcn_exp2f(Ar[hcol[tau]] * c1 - m) : 0.0f;
+        const float e = tau < hl ? __builtin_amdgcn_exp2f(Ar[col(tau)] * c1 - m) : 0.0f;
         sum += e;
-        s2 = fmaf(e, tau < hl - 1 ? shist[tau < hl - 1 ? tau : 0] : 0.0f, s2);
-        alpha[tau] = e;
+        const float sv = tau < pos - 1 ? shist[tau] : tau == pos - 1 ? bst_prev : 0.0f;
+        s2 = fmaf(e, sv, s2);
+        alphaw[tau] = e;
       }
     }
     wave_sum2_fused(sum, s2);
-    if (lane == 0) {
-      sm[0] = __builtin_amdgcn_rcpf(sum);
-      sm[1] = s2;
-      sm[2] = __builtin_amdgcn_exp2f(r_new * c1 - m);
-    }
+    s_inv = __builtin_amdgcn_rcpf(sum);
+    s_st = s2;
+    s_enew = __builtin_amdgcn_exp2f(r_new * c1 - m);
   };
 
-  // Load entry (row r, column c) as the newest: this thread's A value and the
-  // B values of its columns (left in flight); wave 0 also computes the next
-  // step's softmax.
-  auto load_entry = [&](int r, int c) {
-    const float* Ar = A + (int64_t)r * ld;
-    const float* Br = Bm + (int64_t)r * ld;
-    const int pos = hl;
-    a_main = mcol ? Ar[j] : 0.0f;
-    b_main = mcol ? Br[j] : 0.0f;
-    if (SEC) {
-      a_sec = scol ? Ar[js] : 0.0f;
-      b_sec = scol ? Br[js] : 0.0f;
-    }
-    a_stop = Ar[n];
-    b_stop = Br[n];
-    {
-      const int k = pos >> 6;
-      const bool mine = lane == (pos & 63);
-      if (__builtin_amdgcn_readfirstlane(k == 0) && mine) hc0 = c;
-      if (__builtin_amdgcn_readfirstlane(k == 1) && mine) hc1 = c;
-      if (__builtin_amdgcn_readfirstlane(k == 2) && mine) hc2 = c;
-      if (__builtin_amdgcn_readfirstlane(k == 3) && mine) hc3 = c;
-    }
-    if (tid == 0) hcol[pos] = c;
-    ecol = c;
-    hl = pos + 1;
-    if (wave == 0) softmax_w0(Ar);
-  };
-  // Store the newest entry's B values into the history (before the next one).
+  // g = 1: store the newest entry's B values into the history (before the
+  // next entry replaces them).
   auto store_entry = [&]() {
     const int pos = hl - 1;
     if (pos < RREG) hput(pos, b_main);
@@ -424,14 +421,48 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     if (swave && pos < ks && sq == ((pos >> 2) & 3))
       hsec[(((pos >> 4) * 256 + opaque(tid)) << 2) + (pos & 3)] = b_sec;
     if (tid == 0) shist[pos] = b_stop;
-    if (wave == 0) {
-      const int k = pos >> 6;
-      const bool mine = lane == (pos & 63);
-      if (__builtin_amdgcn_readfirstlane(k == 0) && mine) sh0 = b_stop;
-      if (__builtin_amdgcn_readfirstlane(k == 1) && mine) sh1 = b_stop;
-      if (__builtin_amdgcn_readfirstlane(k == 2) && mine) sh2 = b_stop;
-      if (__builtin_amdgcn_readfirstlane(k == 3) && mine) sh3 = b_stop;
+    put4(sh0, sh1, sh2, sh3, pos, b_stop);
+  };
+
+  // g = 1: entry (row r, column c) becomes the newest.  Every load of the step
+  // is issued first, so they share one memory round trip: this thread's A and
+  // B values of the new row (columns without a candidate read column 0 and
+  // are never used), the STOP column, and the history scores gathered from the
+  // new row at the history columns (slots past the history read a valid
+  // column and are masked).  The bookkeeping runs while they are in flight;
+  // then every wave computes the history softmax.
+  auto advance = [&](int r, int c) {
+    const float* Ar = A + (int64_t)r * ld;
+    const float* Br = Bm + (int64_t)r * ld;
+    const float na = Ar[jc], nb = Br[jc];
+    float nas = 0.0f, nbs = 0.0f;
+    if (SEC) {
+      nas = Ar[jsc];
+      nbs = Br[jsc];
     }
+    const float na_stop = Ar[n], nb_stop = Br[n];
+    const float r_new = Ar[c];
+    float r0 = 0.0f, r1 = 0.0f, r2 = 0.0f, r3 = 0.0f;
+    if (hl < 256) {
+      r0 = Ar[hc0];
+      r1 = Ar[hc1];
+      r2 = Ar[hc2];
+      r3 = Ar[hc3];
+    }
+    const float bst_prev = b_stop;
+    const int pos = hl;
+    if (pos > 0) store_entry();
+    put4(hc0, hc1, hc2, hc3, pos, c);
+    if (tid == 0) hcol[pos] = c;
+    ecol = c;
+    hl = pos + 1;
+    a_main = na;
+    b_main = nb;
+    a_sec = nas;
+    b_sec = nbs;
+    a_stop = na_stop;
+    b_stop = nb_stop;
+    softmax_all(Ar, r0, r1, r2, r3, r_new, bst_prev);
   };
 
   // Grouped rounds: history softmax for the mean query of the newest group,
@@ -619,7 +650,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     cols[0] = n + 1;
     load_group(rows, cols, 1);
   } else {
-    load_entry(n, n + 1);   // history entry 0 is START: row n of A and B, column n + 1
+    advance(n, n + 1);   // history entry 0 is START: row n of A and B, column n + 1
   }
   lds_barrier();
   bool selected = false, sel_sec = false;
@@ -655,8 +686,8 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
   for (int t = 1; t <= cap; ++t) {
     const int par = t & 1;
     if (traj && tj_pending) traj_finish();
-    const float inv = sm[0], st = sm[1];
-    const float e_new = GROUPED ? 0.0f : sm[2];
+    const float inv = GROUPED ? sm[0] : s_inv, st = GROUPED ? sm[1] : s_st;
+    const float e_new = GROUPED ? 0.0f : s_enew;
 
     // ---- logits of the lane-owned columns: older entries from the history
     // tiers (the newest entry's slots still hold zero), then the newest.
@@ -664,7 +695,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     {
       // Weights come from LDS 16 at a time, the next 16 requested before the
       // current 16 are used (alternating register sets, no copies).
-      const float4* a4 = reinterpret_cast<const float4*>(alpha);
+      const float4* a4 = reinterpret_cast<const float4*>(alphaw);
       float4 xa[2][4];
       xa[0][0] = a4[0]; xa[0][1] = a4[1]; xa[0][2] = a4[2]; xa[0][3] = a4[3];
 #pragma unroll
@@ -696,7 +727,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
         float4 av[4], hv[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          av[u] = *reinterpret_cast<const float4*>(alpha + tau + 4 * u);
+          av[u] = *reinterpret_cast<const float4*>(alphaw + tau + 4 * u);
           hv[u] = *reinterpret_cast<const float4*>(hj + tau + 4 * u);
         }
 #pragma unroll
@@ -708,7 +739,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
         }
       }
       for (; tau < lend; tau += 4) {
-        const float4 av = *reinterpret_cast<const float4*>(alpha + tau);
+        const float4 av = *reinterpret_cast<const float4*>(alphaw + tau);
         const float4 hv = *reinterpret_cast<const float4*>(hj + tau);
         acc = fmaf(av.x, hv.x, acc);
         accb = fmaf(av.y, hv.y, accb);
@@ -723,7 +754,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
           av[u] = 0.0f;
           if (tau + u < hl - ng) {
             const int c = hcol[tau + u];
-            av[u] = alpha[tau + u];
+            av[u] = alphaw[tau + u];
             if (mcol) hv[u] = Bm[(int64_t)(c == n + 1 ? n : c) * ld + j];
           }
         }
@@ -762,7 +793,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
       const int last = hl - ng;                // the newest entries are added below
       const int lend = last < ks ? last : ks;
       const int st4 = opaque(tid);                 // 4 scl + sq in waves 0-3
-      const float* as = alpha + 4 * (st4 & 3);
+      const float* as = alphaw + 4 * (st4 & 3);
       const float* hs = hsec + st4 * 4;
       for (int k0 = 0; 16 * k0 < lend; k0 += 4) {
         float4 av[4], hv[4];
@@ -784,7 +815,7 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
       for (int tau = ks + sq; tau < last; tau += 4) {
         const int c = hcol[tau];
         const float hv = scol ? Bm[(int64_t)(c == n + 1 ? n : c) * ld + js] : 0.0f;
-        acc2 = fmaf(alpha[tau], hv, acc2);
+        acc2 = fmaf(alphaw[tau], hv, acc2);
       }
       // quad sum of the four quarters: (q0 + q1) + (q2 + q3) in every lane of
       // the quad (each addition is commutative, so all four agree bit for bit)
@@ -920,37 +951,51 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
       }
       lds_barrier();     // the next softmax is in LDS
     } else {
-      // ---- this wave's best candidate (lowest index on ties) into the key
+      // ---- this wave's best candidate (lowest index on ties) as its key in
+      // the step's slots (wave 0 folds STOP in); the slots of this parity are
+      // written again two steps on, after every wave has read them and passed
+      // the next barrier
       const bool valid = mcol && !selected;
       const float v = valid ? lj : -INFINITY;
       const float vmax = wave_max_fused(swave ? fmaxf(v, ls) : v);
       int i1 = -1;
+      unsigned long long wkey = 0ull;
       if (vmax > -INFINITY) {
         const uint64_t m1 = __ballot(valid && v == vmax);
         if (m1) i1 = wave * 64 + __ffsll((unsigned long long)m1) - 1;
         else if (SEC) i1 = 512 + (wave << 4) + ((__ffsll((unsigned long long)__ballot(ls == vmax)) - 1) >> 2);
-        if (lane == 0) atomicMax(&key[par], (unsigned long long)cand_key(vmax, i1));
+        wkey = cand_key(vmax, i1);
       }
-      if (tid == 0 && l_stop > -INFINITY && !full)
-        atomicMax(&key[par], (unsigned long long)cand_key(l_stop, n));
+      if (wave == 0 && l_stop > -INFINITY && !full) {
+        const unsigned long long sk = cand_key(l_stop, n);
+        wkey = sk > wkey ? sk : wkey;
+      }
+      unsigned long long* kp = key + par * 16;
+      if (lane == 0) kp[wave] = wkey;
       if (TRACE) {
         // runner-up of this wave: the best candidate other than i1
         const float w1 = valid && j != i1 ? lj : -INFINITY;
         const float w2 = SEC && js != i1 ? ls : -INFINITY;
         const float v2 = wave_max_fused(fmaxf(w1, w2));
-        if (lane == 0) red[wave] = make_float4(vmax, __int_as_float(i1), v2, 0.0f);
+        if (lane == 0) red[par * 16 + wave] = make_float4(vmax, __int_as_float(i1), v2, 0.0f);
       }
       lds_barrier();
 
-      // ---- the decision (every wave reads the same key)
-      const uint64_t kk = key[par];
+      // ---- the decision: the largest key of the step (every wave reads them all)
+      unsigned long long kk = 0ull;
+      for (int w = 0; w < W; ++w) {
+        const unsigned long long kw = kp[w];
+        kk = kw > kk ? kw : kk;
+      }
+      // uniform: into scalar registers, so the row addresses are scalar work
+      kk = ((unsigned long long)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(kk >> 32)) << 32) |
+           (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)kk);
       const int a = kk ? key_index(kk) : n;       // no finite candidate: STOP
-      if (tid == 0) key[par ^ 1] = 0ull;          // next step's key (last read a step ago)
       if (TRACE && tid == 0 && t <= p.trace_steps) {
         // runner-up: the largest value among the candidates other than a
         float r2 = a == n ? -INFINITY : l_stop;
         for (int w = 0; w < W; ++w) {
-          const float4 r = red[w];
+          const float4 r = red[par * 16 + w];
           r2 = fmaxf(r2, __float_as_int(r.y) == a ? r.z : r.x);
         }
         float* rec = p.trace + ((int64_t)g * p.trace_steps + (t - 1)) * p.trace_w;
@@ -976,11 +1021,9 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
       ++kept;
       if (j == a) selected = true;
       if (SEC && js == a) sel_sec = true;
-      if (!no_history) {
-        store_entry();
-        load_entry(a, a);
-      }
-      lds_barrier();     // the next softmax is in LDS
+      // the next step's weights: every wave computes its own, so no second
+      // barrier is needed
+      if (!no_history) advance(a, a);
     }
   }
 
@@ -1245,7 +1288,8 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   // LDS: fixed arrays, then wave 0's second-column history (all of it if it
   // fits), then the lane-owned tier past the registers; entries beyond either
   // are read again from the Gram buffer.
-  const size_t fixed = (size_t)SelLds(W, 0, 0, p.alpha_ld, p.hcap).total;
+  const int copies = grouped ? 1 : W;              // softmax weight copies
+  const size_t fixed = (size_t)SelLds(W, 0, 0, p.alpha_ld, p.hcap, copies).total;
   size_t room = fixed < (size_t)kLdsBytes ? (size_t)kLdsBytes - fixed : 0;
   int ks = 0;
   if (sec) {
@@ -1266,7 +1310,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   }
   p.lt = lt;
   p.ks = ks;
-  const size_t lds = (size_t)SelLds(W, lt, ks, p.alpha_ld, p.hcap).total;
+  const size_t lds = (size_t)SelLds(W, lt, ks, p.alpha_ld, p.hcap, copies).total;
   if (lds > (size_t)kLdsBytes) return hipErrorInvalidValue;
 
   const void* fn = nullptr;
