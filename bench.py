@@ -159,7 +159,7 @@ def _oracle_sample(w, b_stop, budget_s, threads):
                       f"float64, {elapsed:.1f} s"}
 
 
-def steady_pass(w, R, b_stop, hip, stream, t_scan_roof, ref_kept, steps=10, warmup=2):
+def steady_pass(w, R, b_stop, hip, stream, t_scan_roof, ref_kept, longest, steps=10, warmup=2):
     """Secondary, labelled steady-state figure for the selection stage: R copies
     of the batch in one call of each stage, so the recurrence runs R times as
     many episodes at once (up to one per compute unit) and the per-batch select
@@ -199,6 +199,7 @@ def steady_pass(w, R, b_stop, hip, stream, t_scan_roof, ref_kept, steps=10, warm
     return {"copies": R, "images": R * w.batch, "episodes": int(lay.grp_off.size - 1),
             "select_us": round(sel, 2), "gram_us": round(gram, 2), "recurrence_us": round(rec, 2),
             "select_us_per_batch": round(sel / R, 2),
+            "recurrence_us_per_step_longest_episode": round(rec / max(1, longest), 3),
             "frac_keyscan_roofline": round(R * t_scan_roof / (sel * 1e-6), 4),
             "note": "secondary figure: R copies of the batch per call of each stage; "
                     "not the headline value"}
@@ -456,9 +457,11 @@ def main(argv=None):
     ap.add_argument("--trajectory", type=float, nargs=2, metavar=("TAU", "BETA"), default=None,
                     help="also time the selection with the trajectory sums of Eqs. 5-7 over the "
                          "full rollout (stepprune_select_trajectory) against the plain selection")
-    ap.add_argument("--steady", type=int, default=0, metavar="R",
+    ap.add_argument("--steady", type=int, default=-1, metavar="R",
                     help="also time the selection stage on R copies of the batch in one call "
-                         "(R x the episodes at once): a secondary steady-state figure")
+                         "(R x the episodes at once): a secondary steady-state figure; -1 (the "
+                         "default): 256 / episodes copies when the batch has fewer than 128 "
+                         "episodes (16 for the 16 x 576 batch), none otherwise; 0: none")
     ap.add_argument("--denoise", action="store_true",
                     help="also time the training pathway's noise gate and masked denoiser "
                          "(stepprune_gate_denoise) on the batch's visual tokens")
@@ -767,9 +770,10 @@ def main(argv=None):
         if peaks.get("bf16_matmul_TFLOPs"):
             out["gate_denoise"]["frac_measured_peak"] = round(
                 out["gate_denoise"]["achieved_tflops"] / peaks["bf16_matmul_TFLOPs"], 4)
-    if args.steady > 0:
-        out["select_steady"] = steady_pass(w, args.steady, b_stop, hip, stream, t_scan_roof,
-                                           run.kept_lists())
+    steady = args.steady if args.steady >= 0 else (max(1, N_CU // s.G) if s.G < 128 else 0)
+    if steady > 0:
+        out["select_steady"] = steady_pass(w, steady, b_stop, hip, stream, t_scan_roof,
+                                           run.kept_lists(), max(steps_g))
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, lay, b_stop, args.cpu_budget)
         one = cpu_baseline(w, lay, b_stop, args.cpu_budget * 0.5, single_thread=True)

@@ -651,6 +651,10 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     load_group(rows, cols, 1);
   } else {
     advance(n, n + 1);   // history entry 0 is START: row n of A and B, column n + 1
+    // Consume START's loaded values here: a load still pending at the loop's
+    // entry would make every step wait for its first load before the history
+    // bookkeeping.
+    asm volatile("" ::"v"(a_main), "v"(b_main), "v"(a_sec), "v"(b_sec), "v"(a_stop), "v"(b_stop));
   }
   lds_barrier();
   bool selected = false, sel_sec = false;
