@@ -16,6 +16,7 @@ Modules
   trajectory   the trajectory sums of the training surrogate (Eqs. 5-7)
   compaction   Algorithm 1 step 5: gather of kept tokens ahead of the prompt
   denoise      the training pathway's noise gate (Eq. 9) and masked denoiser
+  encoder      the cross-modal input encoder (Eq. 3)
   calibration  the STOP bias that gives a target mean retained count
 
 Every function states the passage it follows.  Readings of points the paper
@@ -29,6 +30,7 @@ from .trajectory import TrajectoryResult, step_distribution, aggregate, run_traj
 from .compaction import compact
 from .calibration import stop_thresholds, choose_stop_bias
 from .denoise import DenoiserParams, vp_gate, denoise, gate_denoise
+from .encoder import EncoderBlock, text_projection, encode
 
 __all__ = [
     "round_bf16", "round_f32", "round_to", "project", "text_context", "layer_norm",
@@ -36,4 +38,5 @@ __all__ = [
     "compact", "stop_thresholds", "choose_stop_bias",
     "TrajectoryResult", "step_distribution", "aggregate", "run_trajectory",
     "DenoiserParams", "vp_gate", "denoise", "gate_denoise",
+    "EncoderBlock", "text_projection", "encode",
 ]
