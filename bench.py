@@ -30,6 +30,7 @@ host's cores over a bounded sample of the same batch.
 
     python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--streams 3] [--slots 4]
                     [--workload llava15_bf16] [--trajectory TAU BETA] [--steady R] [--denoise]
+                    [--encoder] [--lds-probe] [--shared-inputs]
 """
 import argparse
 import ctypes
@@ -249,6 +250,63 @@ def gate_denoise_pass(w, K, hip, stream, mfma_peak):
             "bound": "mfma"}
 
 
+def encoder_pass(w, K, hip, stream, mfma_peak, causal=False):
+    """The cross-modal input encoder (stepprune_encode, Eq. 3) on the batch:
+    mean time of the whole call over K calls (HIP events around it) and its
+    matrix throughput.  Algorithmic flop: the text product 2 T_txt d_text d;
+    per block 24 S d^2 for the four products over the S = T_vis + T_txt
+    sequence rows and 4 S_b^2 d for each image's attention (q k^T and p v;
+    half of it when causal)."""
+    import numpy as np
+    import torch
+    from paper_2609_13804_amd import binding as sp
+    from paper_2609_13804_amd import workloads as W
+    lay = W.make_layout(w)
+    inp = W.make_inputs(w)
+    params = W.make_encoder_inputs(w)
+    dev = torch.device("cuda")
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev, torch.bfloat16)
+    f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+    B = lay.batch
+    T_vis, T_txt = int(lay.img_off[-1]), int(lay.text_off[-1])
+    seqs = np.diff(lay.img_off).astype(np.int64) + np.diff(lay.text_off)
+    max_seq = int(seqs.max())
+    X, E, Wp = bf(inp["X"]), bf(inp["E_text"]), bf(params["W_p"])
+    blk = [{k: (bf(v) if k.startswith("W_") else f32(v)) for k, v in b.items()}
+           for b in params["blocks"]]
+    del inp, params
+    io = torch.from_numpy(lay.img_off.astype(np.int32)).to(dev)
+    to = torch.from_numpy(lay.text_off.astype(np.int32)).to(dev)
+    dm = sp.dims(w.d, w.d_text, w.h, sp.SP_BF16)
+    ws_bytes = sp.stepprune_workspace_bytes(sp.STAGE_ENCODE, dm, T_vis, T_txt, B, 0, max_seq, 0)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device=dev)
+    H = torch.empty((T_vis, w.d), dtype=torch.bfloat16, device=dev)
+    blocks = sp.encoder_blocks(blk)
+    flags = sp.SP_ENC_CAUSAL if causal else 0
+    call = lambda ev=None: sp.stepprune_encode(dm, X, T_vis, io, B, E, to, T_txt, Wp, 1.0, blocks,
+                                               max_seq, flags, H, ws, ws_bytes, stream, events=ev)
+    for _ in range(3):
+        call()
+    evs = [(hip.create(), hip.create()) for _ in range(K)]
+    for e in evs:
+        call([e[0], e[1]])
+    torch.cuda.synchronize()
+    if sp.stepprune_read_device_error(ws):
+        raise RuntimeError("device error in the encoder")
+    us = float(np.mean([1e3 * hip.ms(a, b) for a, b in evs]))
+    for a, b in evs:
+        hip.destroy(a)
+        hip.destroy(b)
+    S = T_vis + T_txt
+    attn = float((seqs.astype(np.float64) ** 2).sum()) * 4.0 * w.d * (0.5 if causal else 1.0)
+    flop = 2.0 * T_txt * w.d_text * w.d + W.ENCODER_BLOCKS * (24.0 * S * w.d * w.d + attn)
+    achieved = flop / (us * 1e-6) / 1e12
+    return {"images": B, "sequence_rows": S, "d": w.d, "heads": w.d // 128, "us": round(us, 2),
+            "us_per_image": round(us / B, 2), "attention": "causal" if causal else "bidirectional",
+            "algorithmic": f"{flop * 1e-12:.4f} TFLOP", "achieved_tflops": round(achieved, 2),
+            "frac": round(achieved / mfma_peak, 4), "bound": "mfma"}
+
+
 def host_info():
     """The host the CPU baseline ran on: CPU model, cores visible to this
     process, and the BLAS library NumPy's products use with its thread count."""
@@ -462,6 +520,9 @@ def main(argv=None):
                          "(R x the episodes at once): a secondary steady-state figure; -1 (the "
                          "default): 256 / episodes copies when the batch has fewer than 128 "
                          "episodes (16 for the 16 x 576 batch), none otherwise; 0: none")
+    ap.add_argument("--encoder", action="store_true",
+                    help="also time the cross-modal input encoder of Eq. 3 (stepprune_encode, two "
+                         "blocks over each image's visual and text tokens) on the batch")
     ap.add_argument("--denoise", action="store_true",
                     help="also time the training pathway's noise gate and masked denoiser "
                          "(stepprune_gate_denoise) on the batch's visual tokens")
@@ -763,6 +824,13 @@ def main(argv=None):
     }
     if args.trajectory is not None:
         out["trajectory"] = trajectory_pass(run, args.trajectory, K, hip)
+    if args.encoder:
+        if w.dtype != "bf16" or w.d % 128:
+            raise SystemExit("--encoder needs a bfloat16 workload with d a multiple of 128")
+        out["encoder"] = encoder_pass(w, K, hip, stream, mfma_peak)
+        if peaks.get("bf16_matmul_TFLOPs"):
+            out["encoder"]["frac_measured_peak"] = round(
+                out["encoder"]["achieved_tflops"] / peaks["bf16_matmul_TFLOPs"], 4)
     if args.denoise:
         if w.dtype != "bf16":
             raise SystemExit("--denoise needs a bfloat16 workload")

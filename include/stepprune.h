@@ -13,10 +13,12 @@
  *                      episode, kept indices restored to native order;
  *   stepprune_compact  step 5: physical gather of the kept tokens ahead of the
  *                      prompt into a padded or packed prefill buffer.
- * Beside them, for the training pathway (Section "Trajectory-Aware
- * Differentiable Optimization"): stepprune_select_trajectory (the trajectory
- * sums of Eqs. 5-7) and stepprune_gate_denoise (the noise gate of Eq. 9 and
- * the locally masked denoiser).
+ * Beside them: stepprune_encode, the cross-modal input encoder of Eq. 3 that
+ * turns X into the candidate tokens H ahead of step 1; and, for the training
+ * pathway (Section "Trajectory-Aware Differentiable Optimization"),
+ * stepprune_select_trajectory (the trajectory sums of Eqs. 5-7) and
+ * stepprune_gate_denoise (the noise gate of Eq. 9 and the locally masked
+ * denoiser).
  *
  * Conventions shared by every call
  *  - Pointers are DEVICE pointers unless marked (host).  All row-major.
@@ -372,9 +374,75 @@ sp_status stepprune_gate_denoise(const sp_dims* dims, const void* X, int64_t T,
                                  void* out, void* ws, size_t ws_bytes,
                                  const hipEvent_t* events, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * The cross-modal input encoder of Eq. 3 (Section "Conditional Sequential
+ * Pointer Policy", paragraph "Cross-Modal Input Encoder"):
+ *
+ *   E~_b = g_text LN(E_b W_p^T)                (LayerNorm without scale or
+ *                                               shift, biased variance, eps 1e-5)
+ *   H_b  = Enc([X_b; E~_b])[first N_b rows]
+ *
+ * for every image b.  Enc is two pre-norm transformer blocks of width d:
+ *   h = x + W_o MHA(LN1(x)) + b_o,   y = h + W_2 GELU(W_1 LN2(h) + b_1) + b_2,
+ * LayerNorm with scale and shift (eps 1e-6), multi-head attention with heads
+ * of width 128 over q, k, v = LN1(x) W_qkv^T + b_qkv (rows [0, d) query,
+ * [d, 2d) key, [2d, 3d) value of W_qkv; head j takes columns [128 j, 128 j +
+ * 128) of each), scores scaled by 128^(-1/2), over the image's whole sequence
+ * (bidirectional, the paper's default; SP_ENC_CAUSAL: token i attends to
+ * tokens j <= i, visual tokens first), the MLP 4d wide with the exact GELU.
+ * Images never attend to each other; the text rows are not output.  H takes
+ * the place of X as stepprune_project's input (the compaction still gathers
+ * the original X).
+ *
+ * bfloat16 only, d a multiple of 128 up to 4096, d_text a multiple of 64
+ * (SP_EUNSUPPORTED / SP_EINVAL otherwise).  Weights are bfloat16 [out, in],
+ * vectors float32, every array 16-byte aligned.  The residual stream is
+ * float32; the text product, LayerNorm outputs, products, biased q/k/v,
+ * attention probabilities weighting the values, head outputs, the GELU output
+ * and H are rounded once to bfloat16.
+ */
+typedef struct {
+  const float* ln1_g;  /* [d] */
+  const float* ln1_b;  /* [d] */
+  const void* W_qkv;   /* [3d, d] bfloat16 */
+  const float* b_qkv;  /* [3d] */
+  const void* W_o;     /* [d, d] bfloat16 */
+  const float* b_o;    /* [d] */
+  const float* ln2_g;  /* [d] */
+  const float* ln2_b;  /* [d] */
+  const void* W_1;     /* [4d, d] bfloat16 */
+  const float* b_1;    /* [4d] */
+  const void* W_2;     /* [d, 4d] bfloat16 */
+  const float* b_2;    /* [d] */
+} sp_encoder_block;
+
+enum { SP_ENC_CAUSAL = 1u };
+
+/*  X        [T_vis, d] visual tokens, packed by img_off [B+1] (device)
+ *  E_text   [T_txt, d_text] text tokens, packed by text_off [B+1] (device)
+ *  W_p      [d, d_text] bfloat16 text projection; g_text its gain
+ *  blocks   (host) [2] the blocks' parameters, device pointers, none NULL
+ *  max_seq  (host) upper bound on any image's N_b + L_b; an image above it is
+ *           a device error (SP_DEV_GROUP_TOO_LARGE) and its rows of H are
+ *           undefined
+ *  flags    0 or SP_ENC_CAUSAL
+ *  H        out [T_vis, d] bfloat16
+ *  ws       workspace of stepprune_workspace_bytes(4, dims, T_vis, T_txt, B,
+ *           0, max_seq, 0); its first 4 bytes are the device error word
+ *  events   [0] before, [1] after the whole encoder (or NULL)
+ */
+sp_status stepprune_encode(const sp_dims* dims, const void* X, int64_t T_vis,
+                           const int32_t* img_off, int32_t B,
+                           const void* E_text, const int32_t* text_off, int64_t T_txt,
+                           const void* W_p, float g_text,
+                           const sp_encoder_block* blocks, int32_t max_seq, uint32_t flags,
+                           void* H, void* ws, size_t ws_bytes,
+                           const hipEvent_t* events, hipStream_t stream);
+
 /* Workspace bytes for stage `which` (0 project, 1 select, 2 compact, 3 gate
-   and denoiser; for 3, T_vis is the token count T) at the given sizes (host).
-   Returns 0 for invalid arguments. */
+   and denoiser, 4 input encoder; for 3, T_vis is the token count T; for 4,
+   max_group is max_seq) at the given sizes (host).  Returns 0 for invalid
+   arguments. */
 size_t stepprune_workspace_bytes(int32_t which, const sp_dims* dims, int64_t T_vis,
                                  int64_t T_txt, int32_t B, int32_t G,
                                  int32_t max_group, int32_t max_cap);

@@ -22,7 +22,11 @@ STAGE_PROJECT, STAGE_SELECT, STAGE_COMPACT = 0, 1, 2
 
 EXPORTS = ["stepprune_project", "stepprune_select", "stepprune_select_trajectory", "stepprune_compact",
            "stepprune_gate_denoise", "stepprune_workspace_bytes", "stepprune_read_device_error",
-           "stepprune_status_string", "stepprune_select_noalloc"]
+           "stepprune_status_string", "stepprune_select_noalloc", "stepprune_encode"]
+STAGE_ENCODE = 4
+SP_ENC_CAUSAL = 1
+ENCODER_FIELDS = ("ln1_g", "ln1_b", "W_qkv", "b_qkv", "W_o", "b_o", "ln2_g", "ln2_b", "W_1", "b_1",
+                  "W_2", "b_2")
 # size of the fixed device scratch of stepprune_select_noalloc (per GPU)
 NOALLOC_SCRATCH_BYTES = 64 << 20
 STAGE_GATE = 3
@@ -48,6 +52,10 @@ class sp_trajectory(ctypes.Structure):
 class sp_denoiser(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("ln1_g", "ln1_b", "W_v", "b_v", "W_o", "b_o",
                                                "ln2_g", "ln2_b", "W_1", "b_1", "W_2", "b_2")]
+
+
+class sp_encoder_block(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ENCODER_FIELDS]
 
 
 if not os.path.exists(LIB_PATH):
@@ -81,6 +89,10 @@ _lib.stepprune_compact.argtypes = [_DIMS, _P, _P, _P, _P, _P, _P, _P, _I32, _I32
 _lib.stepprune_gate_denoise.restype = _I32
 _lib.stepprune_gate_denoise.argtypes = [_DIMS, _P, _I64, _P, _P, ctypes.POINTER(sp_denoiser), _P,
                                         _P, _SZ, _P, _P]
+_lib.stepprune_encode.restype = _I32
+_lib.stepprune_encode.argtypes = [_DIMS, _P, _I64, _P, _I32, _P, _P, _I64, _P, _F32,
+                                  ctypes.POINTER(sp_encoder_block), _I32, ctypes.c_uint32, _P, _P,
+                                  _SZ, _P, _P]
 _lib.stepprune_workspace_bytes.restype = _SZ
 _lib.stepprune_workspace_bytes.argtypes = [_I32, _DIMS, _I64, _I64, _I32, _I32, _I32, _I32]
 _lib.stepprune_read_device_error.restype = _I32
@@ -208,6 +220,24 @@ def stepprune_gate_denoise(dm, X, T, alpha, eps, params, out, ws, ws_bytes, stre
                                      ctypes.byref(params), _ptr(out), _ptr(ws), ws_bytes,
                                      _events(events), _stream(stream))
     return _check("stepprune_gate_denoise", st, raise_on_error)
+
+
+def encoder_blocks(blocks):
+    """The two blocks' parameters (device tensors by the C field names) as the
+    host array stepprune_encode takes."""
+    arr = (sp_encoder_block * len(blocks))()
+    for i, b in enumerate(blocks):
+        arr[i] = sp_encoder_block(**{k: _ptr(v) for k, v in b.items()})
+    return arr
+
+
+def stepprune_encode(dm, X, T_vis, img_off, B, E_text, text_off, T_txt, W_p, g_text, blocks,
+                     max_seq, flags, H, ws, ws_bytes, stream=None, raise_on_error=True,
+                     events=None):
+    st = _lib.stepprune_encode(ctypes.byref(dm), _ptr(X), T_vis, _ptr(img_off), B, _ptr(E_text),
+                               _ptr(text_off), T_txt, _ptr(W_p), g_text, blocks, max_seq, flags,
+                               _ptr(H), _ptr(ws), ws_bytes, _events(events), _stream(stream))
+    return _check("stepprune_encode", st, raise_on_error)
 
 
 def stepprune_read_device_error(ws, stream=None) -> int:

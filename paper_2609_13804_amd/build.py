@@ -19,7 +19,8 @@ PROBE_LIB = os.path.join(HERE, "libstepprune_probe.so")
 PROBE_SOURCE = "probe.hip"
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["api.hip", "gemm.hip", "select.hip", "text.hip", "compact.hip", "denoise.hip"]
+SOURCES = ["api.hip", "gemm.hip", "select.hip", "text.hip", "compact.hip", "denoise.hip",
+           "encode.hip"]
 # The selection recurrence keeps each column's history in vector registers; let
 # alloca promotion use the whole VGPR budget instead of a quarter of it.
 EXTRA_FLAGS = {"select.hip": ["-mllvm", "-amdgpu-promote-alloca-to-vector-vgpr-ratio=1"]}

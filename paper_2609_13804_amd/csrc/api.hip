@@ -85,6 +85,32 @@ GateWs gate_ws_layout(const sp_dims* d, int64_t T) {
   return w;
 }
 
+// Header, then the encoder's buffers (sp_internal.h, EncodeArgs).
+struct EncodeWs {
+  size_t R, L, A, QKV, HID, Vt, total;
+};
+EncodeWs encode_ws_layout(const sp_dims* d, int64_t T_vis, int64_t T_txt, int B, int max_seq) {
+  EncodeWs w;
+  const size_t S = (size_t)(T_vis + T_txt), dd = (size_t)d->d;
+  w.R = kWsHeaderBytes;
+  w.L = align_up(w.R + S * dd * 4, 256);
+  w.A = align_up(w.L + S * dd * 2, 256);
+  w.QKV = align_up(w.A + S * dd * 2, 256);
+  w.HID = align_up(w.QKV + S * dd * 3 * 2, 256);
+  w.Vt = align_up(w.HID + S * dd * 4 * 2, 256);
+  w.total = align_up(w.Vt + (size_t)B * dd * encode_smax_pad(max_seq) * 2, 256);
+  return w;
+}
+
+// The encoder takes bfloat16, d a multiple of 128 (heads of width 128) up to
+// 4096 (the row kernels keep a row in one wave's registers).
+sp_status check_encode_dims(const sp_dims* d) {
+  sp_status st = check_dims(d);
+  if (st != SP_OK) return st;
+  if (d->dtype != SP_BF16 || d->d % 128 || d->d > 4096) return SP_EUNSUPPORTED;
+  return SP_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -113,6 +139,9 @@ size_t stepprune_workspace_bytes(int32_t which, const sp_dims* dims, int64_t T_v
     case 3:
       if (dims->dtype != SP_BF16 || dims->d > 4096) return 0;
       return gate_ws_layout(dims, T_vis).total;
+    case 4:
+      if (check_encode_dims(dims) != SP_OK || B < 1 || max_group < 1) return 0;
+      return encode_ws_layout(dims, T_vis, T_txt, B, max_group).total;
   }
   return 0;
 }
@@ -377,6 +406,76 @@ sp_status stepprune_read_device_error(void* ws, hipStream_t stream, int32_t* cod
     return SP_EDEVICE;
   }
   return SP_OK;
+}
+
+sp_status stepprune_encode(const sp_dims* dims, const void* X, int64_t T_vis,
+                           const int32_t* img_off, int32_t B, const void* E_text,
+                           const int32_t* text_off, int64_t T_txt, const void* W_p, float g_text,
+                           const sp_encoder_block* blocks, int32_t max_seq, uint32_t flags,
+                           void* H, void* ws, size_t ws_bytes, const hipEvent_t* events,
+                           hipStream_t stream) {
+  const TraceRange range("stepprune_encode");
+  sp_status st = check_encode_dims(dims);
+  if (st != SP_OK) return st;
+  if (T_vis < 0 || T_txt < 0 || B < 1 || max_seq < 1 || !blocks) return SP_EINVAL;
+  if (flags & ~(uint32_t)SP_ENC_CAUSAL) return SP_EINVAL;
+  if (!img_off || !text_off || !W_p || !ws || (T_vis > 0 && (!X || !H)) || (T_txt > 0 && !E_text))
+    return SP_EINVAL;
+  if (!aligned16(X) || !aligned16(E_text) || !aligned16(W_p) || !aligned16(H) || !aligned16(ws))
+    return SP_EINVAL;
+  if (!(g_text == g_text)) return SP_EINVAL;   // NaN
+  for (int k = 0; k < kEncoderBlocks; ++k) {
+    const sp_encoder_block& p = blocks[k];
+    const void* ptrs[] = {p.ln1_g, p.ln1_b, p.W_qkv, p.b_qkv, p.W_o, p.b_o,
+                          p.ln2_g, p.ln2_b, p.W_1, p.b_1, p.W_2, p.b_2};
+    for (const void* q : ptrs)
+      if (!q || !aligned16(q)) return SP_EINVAL;
+  }
+  const EncodeWs w = encode_ws_layout(dims, T_vis, T_txt, B, max_seq);
+  if (ws_bytes < w.total) return SP_EWORKSPACE;
+  char* base = static_cast<char*>(ws);
+  EncodeArgs a;
+  a.d = dims->d;
+  a.d_text = dims->d_text;
+  a.T_vis = T_vis;
+  a.T_txt = T_txt;
+  a.B = B;
+  a.max_seq = max_seq;
+  a.causal = (flags & SP_ENC_CAUSAL) != 0;
+  a.g_text = g_text;
+  a.X = static_cast<const uint16_t*>(X);
+  a.img_off = img_off;
+  a.E = static_cast<const uint16_t*>(E_text);
+  a.text_off = text_off;
+  a.W_p = static_cast<const uint16_t*>(W_p);
+  for (int k = 0; k < kEncoderBlocks; ++k) {
+    const sp_encoder_block& p = blocks[k];
+    EncoderBlockArgs& q = a.blk[k];
+    q.ln1_g = p.ln1_g;
+    q.ln1_b = p.ln1_b;
+    q.W_qkv = static_cast<const uint16_t*>(p.W_qkv);
+    q.b_qkv = p.b_qkv;
+    q.W_o = static_cast<const uint16_t*>(p.W_o);
+    q.b_o = p.b_o;
+    q.ln2_g = p.ln2_g;
+    q.ln2_b = p.ln2_b;
+    q.W_1 = static_cast<const uint16_t*>(p.W_1);
+    q.b_1 = p.b_1;
+    q.W_2 = static_cast<const uint16_t*>(p.W_2);
+    q.b_2 = p.b_2;
+  }
+  a.H = static_cast<uint16_t*>(H);
+  a.R = reinterpret_cast<float*>(base + w.R);
+  a.L = reinterpret_cast<uint16_t*>(base + w.L);
+  a.A = reinterpret_cast<uint16_t*>(base + w.A);
+  a.QKV = reinterpret_cast<uint16_t*>(base + w.QKV);
+  a.HID = reinterpret_cast<uint16_t*>(base + w.HID);
+  a.Vt = reinterpret_cast<uint16_t*>(base + w.Vt);
+  a.err = reinterpret_cast<int32_t*>(base);
+  record_event(events, 0, stream);
+  const hipError_t e = launch_encode(a, stream);
+  record_event(events, 1, stream);
+  return hip_status(e);
 }
 
 sp_status stepprune_gate_denoise(const sp_dims* dims, const void* X, int64_t T,

@@ -13,89 +13,16 @@
 // (x~, then h) stays float32; every product operand and result is bfloat16,
 // rounded once to nearest-even.
 //
-// Row kernels: 16-byte accesses (8 bfloat16 or 4 float32 elements); the
-// LayerNorm kernels run one wave per token row and sum in a fixed order
-// (per-lane partial sums, then a butterfly), so results are deterministic.
+// Row kernels (row_ops.h for the shared pieces): 16-byte accesses (8 bfloat16
+// or 4 float32 elements); the LayerNorm kernels run one wave per token row and
+// sum in a fixed order (per-lane partial sums, then a butterfly), so results
+// are deterministic.  The bias, bias + GELU and residual + LayerNorm kernels
+// serve the input encoder too (launchers below).
 #include "sp_internal.h"
+#include "row_ops.h"
 
 namespace sp {
 namespace {
-
-constexpr int kRowWaves = 4;
-constexpr int kMaxChunks = 8;       // 8-element chunks per lane: d <= 4096
-
-__device__ __forceinline__ float wave_sum(float v) {
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-  return v;
-}
-
-__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
-
-// Eight consecutive elements: bfloat16 in 16 bytes, float32 in 32 bytes.
-__device__ __forceinline__ void load8(const uint16_t* p, float (&v)[8]) {
-  const uint4 u = *reinterpret_cast<const uint4*>(p);
-  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    v[2 * k] = __uint_as_float(w[k] << 16);
-    v[2 * k + 1] = __uint_as_float(w[k] & 0xffff0000u);
-  }
-}
-__device__ __forceinline__ void load8(const float* p, float (&v)[8]) {
-  const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
-  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-}
-__device__ __forceinline__ void store8(uint16_t* p, const float (&v)[8]) {
-  uint32_t w[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k)
-    w[k] = (uint32_t)f32_to_bf16(v[2 * k]) | ((uint32_t)f32_to_bf16(v[2 * k + 1]) << 16);
-  *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
-}
-__device__ __forceinline__ void store8(float* p, const float (&v)[8]) {
-  reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
-  reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
-}
-
-// LayerNorm of a row held as chunks v[i] (elements 8 (lane + 64 i) ..), scaled
-// by g and shifted by b, written as bfloat16.
-__device__ __forceinline__ void ln_store(const float (&v)[kMaxChunks][8], int nch, int d,
-                                         int lane, const float* __restrict__ g,
-                                         const float* __restrict__ b, uint16_t* __restrict__ z) {
-  float s = 0.0f;
-#pragma unroll
-  for (int i = 0; i < kMaxChunks; ++i)
-    if (lane + 64 * i < nch)
-#pragma unroll
-      for (int k = 0; k < 8; ++k) s += v[i][k];
-  const float mean = wave_sum(s) / (float)d;
-  float q = 0.0f;
-#pragma unroll
-  for (int i = 0; i < kMaxChunks; ++i)
-    if (lane + 64 * i < nch)
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const float t = v[i][k] - mean;
-        q = fmaf(t, t, q);
-      }
-  const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)d + kDenoiseLnEps);
-#pragma unroll
-  for (int i = 0; i < kMaxChunks; ++i) {
-    const int c = 8 * (lane + 64 * i);
-    if (c >= d) break;
-    float gg[8], bb[8], o[8];
-    load8(g + c, gg);
-    load8(b + c, bb);
-#pragma unroll
-    for (int k = 0; k < 8; ++k) o[k] = fmaf((v[i][k] - mean) * rstd, gg[k], bb[k]);
-    store8(z + c, o);
-  }
-}
 
 // x~ = sqrt(a) x + sqrt(1 - a) eps into xt (float32), and LN1(x~) into z.
 // One wave per row.
@@ -201,6 +128,28 @@ __global__ __launch_bounds__(256) void out_kernel(const float* __restrict__ h,
 }
 
 }  // namespace
+
+hipError_t launch_row_bias(uint16_t* P, int64_t rows, int n, const float* bias,
+                           hipStream_t stream) {
+  if (rows > 0)
+    hipLaunchKernelGGL(bias_kernel, dim3((unsigned)rows), dim3(256), 0, stream, P, n, bias);
+  return hipGetLastError();
+}
+
+hipError_t launch_row_bias_gelu(uint16_t* H, int64_t rows, int n, const float* bias,
+                                hipStream_t stream) {
+  if (rows > 0)
+    hipLaunchKernelGGL(bias_gelu_kernel, dim3((unsigned)rows), dim3(256), 0, stream, H, n, bias);
+  return hipGetLastError();
+}
+
+hipError_t launch_resid_ln(float* xt, const uint16_t* t, const float* bias, int64_t T, int d,
+                           const float* g, const float* b, uint16_t* z, hipStream_t stream) {
+  if (T > 0)
+    hipLaunchKernelGGL(resid_ln_kernel, dim3((unsigned)((T + kRowWaves - 1) / kRowWaves)),
+                       dim3(64 * kRowWaves), 0, stream, xt, t, bias, T, d, g, b, z);
+  return hipGetLastError();
+}
 
 hipError_t launch_gate_denoise(const DenoiseArgs& a, hipStream_t stream) {
   if (a.T == 0) return hipSuccess;

@@ -155,7 +155,8 @@ hipError_t launch_dense_bf16(const void* A, const void* B, int64_t M, int64_t N,
 // Noise gate and locally masked denoiser (denoise.hip).  Workspace buffers:
 // xt float32 [T, d] (the residual stream), buf_p and buf_q bfloat16 [T, d],
 // hid bfloat16 [T, 4d].
-constexpr float kDenoiseLnEps = 1e-6f;
+// LayerNorm eps of the transformer blocks (the denoiser's and the encoder's).
+constexpr float kBlockLnEps = 1e-6f;
 struct DenoiseArgs {
   int64_t T;
   int d;
@@ -181,5 +182,63 @@ struct DenoiseArgs {
   uint16_t* hid;
 };
 hipError_t launch_gate_denoise(const DenoiseArgs& a, hipStream_t stream);
+
+// Row kernels of denoise.hip, shared with the encoder:
+//   P = bf16(P + bias) and H = bf16(GELU(H + bias)) over rows of width n;
+//   xt = (xt + t) + bias in place and z = LN(xt) (scale g, shift b) over rows
+//   of width d (d <= 4096).
+hipError_t launch_row_bias(uint16_t* P, int64_t rows, int n, const float* bias,
+                           hipStream_t stream);
+hipError_t launch_row_bias_gelu(uint16_t* H, int64_t rows, int n, const float* bias,
+                                hipStream_t stream);
+hipError_t launch_resid_ln(float* xt, const uint16_t* t, const float* bias, int64_t T, int d,
+                           const float* g, const float* b, uint16_t* z, hipStream_t stream);
+
+// Cross-modal input encoder (encode.hip, Eq. 3): two pre-norm transformer
+// blocks over every image's [X_b; g LN(E_b W_p^T)] sequence.  Weights are
+// bfloat16 [out, in]; vectors float32.  Workspace buffers (rows of the
+// S = T_vis + T_txt sequence rows): R float32 [S, d] (the residual stream),
+// L and A bfloat16 [S, d], QKV bfloat16 [S, 3d], HID bfloat16 [S, 4d] (also the
+// text product [T_txt, d]), Vt bfloat16 [B, d, encode_smax_pad(max_seq)].
+constexpr int kEncoderBlocks = 2;
+struct EncoderBlockArgs {
+  const float* ln1_g;
+  const float* ln1_b;
+  const uint16_t* W_qkv;
+  const float* b_qkv;
+  const uint16_t* W_o;
+  const float* b_o;
+  const float* ln2_g;
+  const float* ln2_b;
+  const uint16_t* W_1;
+  const float* b_1;
+  const uint16_t* W_2;
+  const float* b_2;
+};
+struct EncodeArgs {
+  int d, d_text;
+  int64_t T_vis, T_txt;
+  int B;
+  int max_seq;
+  bool causal;
+  float g_text;
+  const uint16_t* X;
+  const int32_t* img_off;
+  const uint16_t* E;
+  const int32_t* text_off;
+  const uint16_t* W_p;
+  EncoderBlockArgs blk[kEncoderBlocks];
+  uint16_t* H;
+  float* R;
+  uint16_t* L;
+  uint16_t* A;
+  uint16_t* QKV;
+  uint16_t* HID;
+  uint16_t* Vt;
+  int32_t* err;
+};
+// Keys per image row of Vt: max_seq rounded up to the transpose tile.
+size_t encode_smax_pad(int max_seq);
+hipError_t launch_encode(const EncodeArgs& a, hipStream_t stream);
 
 }  // namespace sp

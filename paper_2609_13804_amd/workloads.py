@@ -333,6 +333,43 @@ def make_denoiser_inputs(w: Workload, T: int) -> Dict[str, np.ndarray]:
     return out
 
 
+STREAM_ENCODER = 6
+ENCODER_FIELDS = ("ln1_g", "ln1_b", "W_qkv", "b_qkv", "W_o", "b_o", "ln2_g", "ln2_b", "W_1", "b_1",
+                  "W_2", "b_2")
+ENCODER_BLOCKS = 2
+
+
+def make_encoder_inputs(w: Workload) -> Dict[str, object]:
+    """Seeded random-init parameters of the cross-modal input encoder for
+    width w.d: the text projection W_p [d, d_text] and two blocks (weights
+    N(0, 1/fan_in) rounded to bfloat16 in [out, in] layout, biases
+    N(0, 0.02^2), LayerNorm scales 1 + N(0, 0.1^2) and shifts N(0, 0.1^2),
+    float32).  Returns {"W_p": ..., "blocks": [dict, dict]}."""
+    d = w.d
+    rng = _rng(w.cfg_id, STREAM_ENCODER, 0)
+    bf = lambda a: _to_dtype_values(a, "bf16")
+    W_p = bf(rng.standard_normal((d, w.d_text), dtype=np.float32)
+             * np.float32(1.0 / math.sqrt(w.d_text)))
+    shapes = {"W_qkv": (3 * d, d), "W_o": (d, d), "W_1": (4 * d, d), "W_2": (d, 4 * d)}
+    sizes = {"b_qkv": 3 * d, "b_1": 4 * d}
+    blocks = []
+    for _ in range(ENCODER_BLOCKS):
+        blk = {}
+        for name in ENCODER_FIELDS:
+            if name in shapes:
+                n_out, n_in = shapes[name]
+                blk[name] = bf(rng.standard_normal((n_out, n_in), dtype=np.float32)
+                               * np.float32(1.0 / math.sqrt(n_in)))
+            elif name.startswith("ln") and name.endswith("_g"):
+                blk[name] = (1.0 + 0.1 * rng.standard_normal(d)).astype(np.float32)
+            elif name.startswith("ln"):
+                blk[name] = (0.1 * rng.standard_normal(d)).astype(np.float32)
+            else:
+                blk[name] = (0.02 * rng.standard_normal(sizes.get(name, d))).astype(np.float32)
+        blocks.append(blk)
+    return {"W_p": W_p, "blocks": blocks}
+
+
 def load_stop_bias() -> Dict[str, float]:
     if not os.path.exists(STOP_BIAS_FILE):
         return {}

@@ -53,7 +53,8 @@ def test_workspace_bytes(sp):
     gate = sp.stepprune_workspace_bytes(3, dm, 100, 10, 2, 3, 50, 10)   # T = 100 tokens, d = 256
     assert gate >= 256 + 100 * 256 * (4 + 2 + 2 + 8)
     assert sp.stepprune_workspace_bytes(3, _dims(sp, dtype=sp.SP_F32), 100, 10, 2, 3, 50, 10) == 0
-    assert sp.stepprune_workspace_bytes(4, dm, 100, 10, 2, 3, 50, 10) == 0
+    assert sp.stepprune_workspace_bytes(4, dm, 100, 10, 2, 3, 50, 10) > 0       # the encoder
+    assert sp.stepprune_workspace_bytes(5, dm, 100, 10, 2, 3, 50, 10) == 0
     assert sp.stepprune_workspace_bytes(0, _dims(sp, h=100), 100, 10, 2, 3, 50, 10) == 0
 
 
@@ -259,3 +260,29 @@ def test_header_is_plain_c(sp, tmp_path):
                                                        9216, 1024, 16, 16, 576, 192)
     assert int(out[7]) == sp.SP_EINVAL
     assert int(out[8]) == sp.SP_EINVAL
+
+
+def test_encode_validation(sp):
+    blk = sp.encoder_blocks([{k: FAKE for k in sp.ENCODER_FIELDS}] * 2)
+    dm = _dims(sp, d=256, dt=192)
+
+    def call(dm=dm, blocks=blk, max_seq=64, flags=0, ws_bytes=0, X=FAKE, W_p=FAKE):
+        return sp.stepprune_encode(dm, X, 10, FAKE, 1, FAKE, FAKE, 4, W_p, 1.0, blocks, max_seq,
+                                   flags, FAKE + 0x100000, FAKE, ws_bytes, stream=0,
+                                   raise_on_error=False)
+    assert call() == sp.SP_EWORKSPACE                                     # accepted up to the workspace
+    assert call(dm=_dims(sp, d=320, dt=192)) == sp.SP_EUNSUPPORTED       # heads of 128
+    assert call(dm=_dims(sp, d=4224, dt=192)) == sp.SP_EUNSUPPORTED      # d <= 4096
+    assert call(dm=_dims(sp, d=256, dt=192, dtype=sp.SP_F32)) == sp.SP_EUNSUPPORTED
+    assert call(blocks=None) == sp.SP_EINVAL
+    part = sp.encoder_blocks([{k: FAKE for k in sp.ENCODER_FIELDS},
+                              {k: (None if k == "b_2" else FAKE) for k in sp.ENCODER_FIELDS}])
+    assert call(blocks=part) == sp.SP_EINVAL
+    assert call(max_seq=0) == sp.SP_EINVAL
+    assert call(flags=2) == sp.SP_EINVAL
+    assert call(X=None) == sp.SP_EINVAL
+    assert call(W_p=MISALIGNED) == sp.SP_EINVAL
+    need = sp.stepprune_workspace_bytes(4, dm, 10, 4, 1, 0, 64, 0)
+    assert need >= 256 + 14 * 256 * (4 + 2 + 2 + 6 + 8)
+    assert call(ws_bytes=need - 1) == sp.SP_EWORKSPACE
+    assert sp.stepprune_workspace_bytes(4, dm, 10, 4, 1, 0, 0, 0) == 0     # max_seq >= 1
