@@ -116,7 +116,12 @@ sp_status check_encode_dims(const sp_dims* d) {
 extern "C" {
 
 const char* stepprune_status_string(sp_status s) {
-  switch (s) {
+  // A C caller may pass any int: read its bytes, since loading an enumeration
+  // outside its enumerators' range is undefined in C++.
+  static_assert(sizeof(sp_status) == sizeof(int32_t), "sp_status is int-sized");
+  int32_t v;
+  memcpy(&v, &s, sizeof(v));
+  switch (v) {
     case SP_OK: return "ok";
     case SP_EINVAL: return "invalid argument";
     case SP_EUNSUPPORTED: return "unsupported argument";
