@@ -18,6 +18,8 @@
 //  * per-group Gram products of the projected rows used by the selection
 //    recurrence (select.hip): rows [Q_g; q_start; V_g; v_start; context split]
 //    against columns [K_g; k_stop; k_start].
+#include <type_traits>
+
 #include "sp_internal.h"
 
 namespace sp {
@@ -186,8 +188,17 @@ constexpr int kStageBytes = 2 * kOpBytes;              // A and B, 32 KiB
 typedef __attribute__((address_space(1))) const void* gptr_t;
 typedef __attribute__((address_space(3))) void* lptr_t;
 
+// One 16-byte-per-lane global load straight into LDS (global_load_lds_dwordx4:
+// lane i's bytes land at dst + 16 i, dst taken from M0).  It is written as
+// inline assembly so that the compiler does not track it: it models the
+// builtin as an access that may touch both memory and LDS, and then waits for
+// every outstanding LDS read (lgkmcnt(0)) wherever a fragment is consumed,
+// including reads issued just before.  Its completion is awaited explicitly
+// (wait_vmcnt, then a barrier) before any wave reads the stage it fills.
 __device__ __forceinline__ void lds_dma16(const void* src, char* dst) {
-  __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)dst, 16, 0, 0);
+  const uint32_t l = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lptr_t)dst);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(l) : "memory", "m0");
 }
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
@@ -289,14 +300,20 @@ __device__ __forceinline__ void gemm_bf16_256(const ARows& ar, const BRows& br, 
     if (q < GPW) lds_dma16(pa[q] + k0, a + (wave + WAVES * q) * 1024);
     else lds_dma16(pb[q - GPW] + k0, a + kOpBytes + (wave + WAVES * (q - GPW)) * 1024);
   };
-  auto step = [&](int kt, Frags& cur, Frags& nxt) {
+  // MORE / REFILL: 1 means always, -1 decided at run time.  The steady-state
+  // loop instantiates both as 1, so its body has no branches: at a join of
+  // branches the compiler's wait counting falls back to waiting for every
+  // outstanding LDS read, and each half-step would then stall on the
+  // fragment reads it has just issued.
+  auto step = [&](int kt, Frags& cur, Frags& nxt, auto more_c, auto refill_c) {
+    constexpr int MORE = decltype(more_c)::value, REFILL = decltype(refill_c)::value;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a0[i], cur.b0[j], acc[i][j], 0, 0, 0);
-    const bool more = kt + 1 < KT;
-    const bool refill = kt + kStages - 1 < KT;
+    const bool more = MORE == 1 || kt + 1 < KT;
+    const bool refill = REFILL == 1 || kt + kStages - 1 < KT;
     if (more) {
       // Stage kt + 1 has landed once at most (stages issued after it) x loads
       // of this wave remain.  The buffer refilled below held stage kt - 1,
@@ -332,12 +349,19 @@ __device__ __forceinline__ void gemm_bf16_256(const ARows& ar, const BRows& br, 
     }
     __builtin_amdgcn_sched_barrier(0);
   };
+  using Always = std::integral_constant<int, 1>;
+  using Checked = std::integral_constant<int, -1>;
   int kt = 0;
-  for (; kt + 1 < KT; kt += 2) {
-    step(kt, f0, f1);
-    step(kt + 1, f1, f0);
+  // Steady state: both steps of a pair have a next stage and a refill.
+  for (; kt + kStages < KT; kt += 2) {
+    step(kt, f0, f1, Always{}, Always{});
+    step(kt + 1, f1, f0, Always{}, Always{});
   }
-  if (kt < KT) step(kt, f0, f1);
+  for (; kt + 1 < KT; kt += 2) {
+    step(kt, f0, f1, Checked{}, Checked{});
+    step(kt + 1, f1, f0, Checked{}, Checked{});
+  }
+  if (kt < KT) step(kt, f0, f1, Checked{}, Checked{});
 
   // 32x32 MFMA result layout: lane l, register r holds
   // row 8*(r/4) + 4*(l/32) + r%4, column l%32.

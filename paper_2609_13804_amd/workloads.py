@@ -19,10 +19,16 @@ available, so seeded tensors of the same shapes stand in for them:
 * sizes (dynamic resolution): N_i = 4 * U{64 .. 1024}.
 
 Every random stream is ``numpy.random.default_rng([260913804, cfg_id, stream,
-index])`` so a given image is identical whatever batch it sits in.  Values are
-drawn in float32 and rounded once (round-to-nearest-even) to bfloat16 for the
-bf16 workloads; the float32 copies handed to the CPU side are those rounded
-values, exactly.
+index])`` so a given image is identical whatever batch it sits in.  The
+one-image float32 workload is keyed 1097: its operating point is 63 retained
+tokens with STOP taken inside the cap of 64 rounds, and the retained counts a
+STOP bias can reach are the breakpoints of the running minimum of the STOP
+margin (see oracle/calibration.py), which depend on the draw (key 1 reaches
+46 at most).  1097 is the first key from 1001 on whose draw reaches 63.
+
+Values are drawn in float32 and rounded once (round-to-nearest-even) to
+bfloat16 for the bf16 workloads; the float32 copies handed to the CPU side are
+those rounded values, exactly.
 """
 from __future__ import annotations
 
@@ -87,7 +93,7 @@ def _add(w: Workload) -> None:
     WORKLOADS[w.name] = w
 
 
-_add(Workload("single_f32", 1, batch=1, d=1024, d_text=1024, h=256, dtype="f32",
+_add(Workload("single_f32", 1097, batch=1, d=1024, d_text=1024, h=256, dtype="f32",
               text_len=32, tokens=(576,), cap=64, layout="padded",
               stop_target=("k_each", 63.0),
               description="1 image, N=576, d=1024, fp32, hidden 256, cap 64"))
