@@ -363,20 +363,59 @@ __device__ __forceinline__ void gemm_bf16_256(const ARows& ar, const BRows& br, 
   }
   if (kt < KT) step(kt, f0, f1, Checked{}, Checked{});
 
-  // 32x32 MFMA result layout: lane l, register r holds
-  // row 8*(r/4) + 4*(l/32) + r%4, column l%32.
+  // Epilogue through LDS: once every wave is past the K loop the operand ring
+  // is free, so the tile is staged there in row-major order and leaves as
+  // 16-byte row chunks (whole cache lines, an eighth or a quarter of the store
+  // instructions of storing the MFMA layout directly).  A float32 tile needs
+  // twice the ring, so it is staged in two passes of 128 rows (the waves with
+  // wm = 0, then wm = 1).  Chunks of rows with bit 2 set are XOR-ed by half a
+  // row of banks: the two rows one write instruction covers (r and r + 4)
+  // then hit different banks.
+  constexpr int E = (int)sizeof(OutT);
+  constexpr int EPC = 16 / E;                              // elements per 16-byte chunk
+  constexpr int CPR = kBN / EPC;                           // chunks per staged row
+  constexpr int ROWS = kStages * kStageBytes / (kBN * E);  // rows staged per pass
+  constexpr int PASSES = kBM / ROWS;
+  constexpr int XS = CPR / 8;
+  constexpr int THREADS = 64 * WAVES;
+  static_assert(ROWS == 128 || ROWS == 256, "one or two staging passes");
+  static_assert(ROWS * CPR % THREADS == 0, "whole chunks per thread");
+  auto sw = [](int lr) { return ((lr >> 2) & 1) * XS; };
+  const bool vec = ((uintptr_t)C % 16 == 0) && ((int64_t)ldc * E % 16 == 0);
+  OutT* T = reinterpret_cast<OutT*>(smem);
+  __syncthreads();
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int p = 0; p < PASSES; ++p) {
+    if (PASSES == 1 || wm == p) {
+      // 32x32 MFMA result layout: lane l, register r holds
+      // row 8*(r/4) + 4*(l/32) + r%4, column l%32.
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int64_t col = n0 + wn * (32 * TN) + j * 32 + (lane & 31);
-      if (col >= N) continue;
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (row < M) C[row * ldc + col] = store_cvt<OutT>(acc[i][j][r]);
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int lr = wm * 128 - p * ROWS + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            const int lc = wn * (32 * TN) + j * 32 + (lane & 31);
+            T[lr * kBN + ((lc / EPC) ^ sw(lr)) * EPC + lc % EPC] = store_cvt<OutT>(acc[i][j][r]);
+          }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < ROWS * CPR / THREADS; ++q) {
+      const int c = tid + THREADS * q, lr = c / CPR, ch = c % CPR;
+      const int64_t row = m0 + p * ROWS + lr, col = n0 + (int64_t)ch * EPC;
+      if (row >= M || col >= N) continue;
+      const OutT* src = T + lr * kBN + (ch ^ sw(lr)) * EPC;
+      OutT* dst = C + row * ldc + col;
+      if (vec && col + EPC <= N) {
+        *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(src);
+      } else {
+        for (int e = 0; e < EPC && col + e < N; ++e) dst[e] = src[e];
       }
     }
+    if (p + 1 < PASSES) __syncthreads();
+  }
 }
 
 // Workgroup w runs on XCD w % 8; give each XCD a contiguous run of tiles (in
