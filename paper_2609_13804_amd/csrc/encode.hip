@@ -21,6 +21,7 @@
 // values, each head's output, the GELU output and H are bfloat16, rounded
 // once to nearest-even.
 #include "sp_internal.h"
+#include "lds_dma.h"
 #include "row_ops.h"
 
 namespace sp {
@@ -33,6 +34,7 @@ constexpr int kHead = 128;                  // head width
 constexpr int kQPerWave = 32;               // queries of one wave (one 32 x 32 MFMA tile)
 constexpr int kAttnWaves = 4;               // 128 queries per workgroup
 constexpr int kKeyBlock = 32;               // keys per online-softmax step
+constexpr int kKeyTile = 64;                // keys per LDS tile of K and V^T
 constexpr int kVtKeys = 64;                 // keys per transpose tile
 constexpr float kTextLnEps = 1e-5f;
 
@@ -179,9 +181,11 @@ __global__ __launch_bounds__(256) void enc_out_kernel(
 
 // ---------------------------------------------------------------- attention
 
-// Vt[b][head][e][k] = V[so_b + k][128 head + e] for k < S_b, 0 up to smax_pad:
-// each head's values transposed (keys contiguous), so the attention's value
-// operand is two 8-byte loads per lane.  One workgroup per 64 keys x 128.
+// Vt[b][head][e][p] = V[so_b + k][128 head + e] for k < S_b, 0 up to smax_pad:
+// each head's values transposed, keys contiguous except that the middle two
+// 4-key quarters of every 16 keys trade places (position p of key k: quarter
+// order 0, 2, 1, 3).  The attention's value operand for a lane half is then
+// one 16-byte chunk (see attn_kernel).  One workgroup per 64 keys x 128.
 __global__ __launch_bounds__(256) void vt_kernel(
     const uint16_t* __restrict__ QKV, int d, int smax_pad, const int32_t* __restrict__ img_off,
     const int32_t* __restrict__ text_off, int max_seq, int64_t S_total, uint16_t* __restrict__ Vt,
@@ -205,23 +209,19 @@ __global__ __launch_bounds__(256) void vt_kernel(
   const int e = tid >> 1, kh = tid & 1;
   uint16_t* dst = Vt + (((int64_t)b * heads + hd) * kHead + e) * smax_pad + k0 + 32 * kh;
 #pragma unroll
-  for (int j = 0; j < 32; j += 8) {
+  for (int j = 0; j < 32; j += 16) {
     const uint16_t* c = &tile[32 * kh + j][e];
-    uint4 w;
-    w.x = (uint32_t)c[0] | ((uint32_t)c[1 * (kHead + 8)] << 16);
-    w.y = (uint32_t)c[2 * (kHead + 8)] | ((uint32_t)c[3 * (kHead + 8)] << 16);
-    w.z = (uint32_t)c[4 * (kHead + 8)] | ((uint32_t)c[5 * (kHead + 8)] << 16);
-    w.w = (uint32_t)c[6 * (kHead + 8)] | ((uint32_t)c[7 * (kHead + 8)] << 16);
-    *reinterpret_cast<uint4*>(dst + j) = w;
+    auto two = [&](int k) {
+      return (uint32_t)c[k * (kHead + 8)] | ((uint32_t)c[(k + 1) * (kHead + 8)] << 16);
+    };
+    // positions 0-7: keys 0-3, 8-11; positions 8-15: keys 4-7, 12-15
+    *reinterpret_cast<uint4*>(dst + j) = make_uint4(two(0), two(2), two(8), two(10));
+    *reinterpret_cast<uint4*>(dst + j + 8) = make_uint4(two(4), two(6), two(12), two(14));
   }
 }
 
 __device__ __forceinline__ bf16x8_t ld16(const uint16_t* p) {
   return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(p));
-}
-__device__ __forceinline__ bf16x8_t ld8x2(const uint16_t* p0, const uint16_t* p1) {
-  const uint2 a = *reinterpret_cast<const uint2*>(p0), c = *reinterpret_cast<const uint2*>(p1);
-  return __builtin_bit_cast(bf16x8_t, make_uint4(a.x, a.y, c.x, c.y));
 }
 __device__ __forceinline__ bf16x8_t pack8(const float* v) {
   uint4 u;
@@ -243,21 +243,29 @@ __device__ __forceinline__ bf16x8_t pack8(const float* v) {
 //   O^T += V^T P: the probabilities a lane holds are its half of the
 //   operand's k slots as they stand (slot 8 (l / 32) + j is key 4 (l / 32) + j
 //   for j < 4 and 8 + 4 (l / 32) + j - 4 for j >= 4, plus 16 for the second
-//   16 keys), and the transposed values are read in that key order.
+//   16 keys), which is the order vt_kernel stores the values in.
+// The workgroup's four waves share the keys and values: 64-key tiles of K
+// (64 x 128) and V^T (128 x 64) pass through LDS, two tiles deep, the next
+// tile loading straight into LDS while the current one is used.
+// LDS rows are 16-byte chunks XOR-swizzled so that each 16-lane pass of a
+// fragment read touches every bank once.
 // Probabilities enter the products rounded to bfloat16; the running maximum
 // rescales the partial sums in float32.
 __global__ __launch_bounds__(64 * kAttnWaves) void attn_kernel(
     const uint16_t* __restrict__ QKV, const uint16_t* __restrict__ Vt, int d, int smax_pad,
     const int32_t* __restrict__ img_off, const int32_t* __restrict__ text_off, int max_seq,
     int64_t S_total, int causal, float c2, uint16_t* __restrict__ O, int32_t* err) {
+  constexpr int kTileBytes = kKeyTile * kHead * 2;                 // one K or V^T tile, 16 KB
+  __shared__ __attribute__((aligned(16))) char smem[2][2][kTileBytes];   // [buffer][K, V^T]
   const int b = blockIdx.z, hd = blockIdx.y, heads = gridDim.y;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int64_t so;
   int S;
-  const bool report = threadIdx.x == 0 && blockIdx.x == 0 && hd == 0;
+  const bool report = tid == 0 && blockIdx.x == 0 && hd == 0;
   if (!sequence_of(img_off, text_off, b, max_seq, S_total, so, S, err, report)) return;
-  const int q0 = blockIdx.x * (kQPerWave * kAttnWaves) + wave * kQPerWave;
-  if (q0 >= S) return;
+  const int qw = blockIdx.x * (kQPerWave * kAttnWaves);            // the workgroup's first query
+  if (qw >= S) return;
+  const int q0 = qw + wave * kQPerWave;                             // this wave's (may be past S)
   const int ql = lane & 31, half = lane >> 5;
   const int64_t ld = 3 * (int64_t)d;
   const uint16_t* Qb = QKV + so * ld + hd * kHead;
@@ -269,55 +277,105 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_kernel(
 #pragma unroll
   for (int s = 0; s < kHead / 16; ++s) qf[s] = ld16(Qb + qr * ld + 16 * s + 8 * half);
 
+  // keys the workgroup needs, and this wave's own limit
+  const int kend_wg = causal ? (S < qw + kQPerWave * kAttnWaves ? S : qw + kQPerWave * kAttnWaves) : S;
+  // (a wave past the sequence only helps load the tiles)
+  const int kend = q0 >= S ? 0 : causal ? (S < q0 + kQPerWave ? S : q0 + kQPerWave) : S;
+  const int tiles = (kend_wg + kKeyTile - 1) / kKeyTile;
+
+  // Tile loads, straight into LDS: a load instruction fills 1 KB, 4 rows of
+  // the K tile (row group w + 4 i of wave w) or 8 rows of the V^T tile; lane
+  // i lands on chunk i % 16 (i % 8) of its row, so it fetches the logical
+  // chunk that the swizzle puts there.  K rows past the sequence read its last
+  // key (masked below); V^T keys past the sequence are zero in Vt up to
+  // smax_pad.
+  static_assert(kKeyTile * kHead * 2 / 1024 == 4 * kAttnWaves, "four row groups per wave");
+  auto issue_tile = [&](int kt, int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int grp = wave + kAttnWaves * i;
+      const int r = 4 * grp + (lane >> 4), ch = (lane & 15) ^ (r & 15);
+      const int k = kt * kKeyTile + r;
+      lds_dma16(Kb + (int64_t)(k < S ? k : S - 1) * ld + 8 * ch, smem[buf][0] + grp * 1024);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int grp = wave + kAttnWaves * i;
+      const int e = 8 * grp + (lane >> 3), ch = (lane & 7) ^ ((e >> 1) & 7);
+      lds_dma16(Vb + (int64_t)e * smax_pad + kt * kKeyTile + 8 * ch, smem[buf][1] + grp * 1024);
+    }
+  };
+  // fragment reads: K rows of key block kb (32 keys) in e-slice s; V^T rows of
+  // e-tile t at the 16-key group g of the tile
+  auto kfrag = [&](int buf, int r, int s) {
+    const int ch = 2 * s + half;
+    return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(smem[buf][0] + r * 256 + ((ch ^ (r & 15)) << 4)));
+  };
+  auto vfrag = [&](int buf, int e, int grp) {
+    const int ch = 2 * grp + half;
+    return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(smem[buf][1] + e * 128 + ((ch ^ ((e >> 1) & 7)) << 4)));
+  };
+
   f32x16_t o[kHead / 32];
 #pragma unroll
   for (int t = 0; t < kHead / 32; ++t)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[t][r] = 0.0f;
   float m = -INFINITY, l = 0.0f;
-  const int kend = causal ? (S < q0 + kQPerWave ? S : q0 + kQPerWave) : S;
-  for (int kb = 0; kb < kend; kb += kKeyBlock) {
-    const int kr = kb + ql < S ? kb + ql : S - 1;
-    f32x16_t st;
+
+  issue_tile(0, 0);
+  wait_vmcnt<0>();
+  __syncthreads();
+  for (int kt = 0; kt < tiles; ++kt) {
+    const int buf = kt & 1;
+    // the other buffer was last read before the previous barrier
+    if (kt + 1 < tiles) issue_tile(kt + 1, buf ^ 1);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) st[r] = 0.0f;
+    for (int sb = 0; sb < kKeyTile / kKeyBlock; ++sb) {
+      const int kb = kt * kKeyTile + sb * kKeyBlock;
+      if (kb >= kend) break;                  // uniform in the wave
+      f32x16_t st;
 #pragma unroll
-    for (int s = 0; s < kHead / 16; ++s)
-      st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld16(Kb + kr * ld + 16 * s + 8 * half), qf[s],
-                                                   st, 0, 0, 0);
-    // Key kb is visible to every query of the wave (kb < S, and kb <= q0 when
-    // causal), so the block maximum is finite.
-    float x[16], bm = -INFINITY;
+      for (int r = 0; r < 16; ++r) st[r] = 0.0f;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = kb + 8 * (r >> 2) + 4 * half + (r & 3);
-      const bool ok = key < S && (!causal || key <= q);
-      x[r] = ok ? st[r] * c2 : -INFINITY;
-      bm = fmaxf(bm, x[r]);
+      for (int s = 0; s < kHead / 16; ++s)
+        st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kfrag(buf, sb * kKeyBlock + ql, s), qf[s], st,
+                                                     0, 0, 0);
+      // Key kb is visible to every query of the wave (kb < S, and kb <= q0 when
+      // causal), so the block maximum is finite.
+      float x[16], bm = -INFINITY;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kb + 8 * (r >> 2) + 4 * half + (r & 3);
+        const bool ok = key < S && (!causal || key <= q);
+        x[r] = ok ? st[r] * c2 : -INFINITY;
+        bm = fmaxf(bm, x[r]);
+      }
+      bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+      const float mn = fmaxf(m, bm);
+      const float sc = __builtin_amdgcn_exp2f(m - mn);     // 0 on the first block
+      float p[16], ls = 0.0f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        p[r] = __builtin_amdgcn_exp2f(x[r] - mn);
+        ls += p[r];
+      }
+      ls += __shfl_xor(ls, 32, 64);
+      l = fmaf(l, sc, ls);
+      m = mn;
+#pragma unroll
+      for (int t = 0; t < kHead / 32; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[t][r] *= sc;
+      const bf16x8_t pb0 = pack8(p), pb1 = pack8(p + 8);
+#pragma unroll
+      for (int t = 0; t < kHead / 32; ++t) {
+        o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(buf, 32 * t + ql, 2 * sb), pb0, o[t], 0, 0, 0);
+        o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(buf, 32 * t + ql, 2 * sb + 1), pb1, o[t], 0, 0, 0);
+      }
     }
-    bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
-    const float mn = fmaxf(m, bm);
-    const float sc = __builtin_amdgcn_exp2f(m - mn);     // 0 on the first block
-    float p[16], ls = 0.0f;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      p[r] = __builtin_amdgcn_exp2f(x[r] - mn);
-      ls += p[r];
-    }
-    ls += __shfl_xor(ls, 32, 64);
-    l = fmaf(l, sc, ls);
-    m = mn;
-#pragma unroll
-    for (int t = 0; t < kHead / 32; ++t)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[t][r] *= sc;
-    const bf16x8_t pb0 = pack8(p), pb1 = pack8(p + 8);
-#pragma unroll
-    for (int t = 0; t < kHead / 32; ++t) {
-      const uint16_t* vr = Vb + (int64_t)(32 * t + ql) * smax_pad + kb + 4 * half;
-      o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld8x2(vr, vr + 8), pb0, o[t], 0, 0, 0);
-      o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld8x2(vr + 16, vr + 24), pb1, o[t], 0, 0, 0);
-    }
+    wait_vmcnt<0>();                         // this wave's loads of the next tile
+    __syncthreads();
   }
   if (q >= S) return;
   // O^T[e][q] in o[t][r]: e = 32 t + 8 (r / 4) + 4 (l / 32) + r % 4

@@ -21,6 +21,7 @@
 #include <type_traits>
 
 #include "sp_internal.h"
+#include "lds_dma.h"
 
 namespace sp {
 namespace {
@@ -184,29 +185,6 @@ __device__ __forceinline__ void gemm_block(const ARows& ar, const BRows& br, int
 constexpr int kBM = 256, kBN = 256, kBK = 32, kStages = 4;
 constexpr int kOpBytes = kBM * kBK * 2;                // one operand tile, 16 KiB
 constexpr int kStageBytes = 2 * kOpBytes;              // A and B, 32 KiB
-
-typedef __attribute__((address_space(1))) const void* gptr_t;
-typedef __attribute__((address_space(3))) void* lptr_t;
-
-// One 16-byte-per-lane global load straight into LDS (global_load_lds_dwordx4:
-// lane i's bytes land at dst + 16 i, dst taken from M0).  It is written as
-// inline assembly so that the compiler does not track it: it models the
-// builtin as an access that may touch both memory and LDS, and then waits for
-// every outstanding LDS read (lgkmcnt(0)) wherever a fragment is consumed,
-// including reads issued just before.  Its completion is awaited explicitly
-// (wait_vmcnt, then a barrier) before any wave reads the stage it fills.
-__device__ __forceinline__ void lds_dma16(const void* src, char* dst) {
-  const uint32_t l = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lptr_t)dst);
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :: "v"(src), "s"(l) : "memory", "m0");
-}
-
-// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
 
 // Byte offset of (row, 16-byte chunk) in a swizzled operand tile (64-byte rows).
 __device__ __forceinline__ int swz(int row, int chunk) {
