@@ -734,10 +734,11 @@ __global__ __launch_bounds__(64 * kGramWaves) void gram_gemm_bf16_kernel(GramArg
                        smem);
 }
 
-// float32 Gram products on the 128 x 128 register-staged core.
+// float32 Gram products on the register-staged core, BM x BN tiles.
+template <int BM, int BN>
 __global__ __launch_bounds__(kThreads) void gram_gemm_f32_kernel(GramArgs a, int per_group,
                                                                 int xcd_grouped) {
-  constexpr int BM = 128, BN = 128, BK = 32;
+  constexpr int BK = 32;
   __shared__ __attribute__((aligned(16))) char smem[Tile<float, BM, BN, BK>::LDS_BYTES];
   int64_t g, t, g0, n;
   int b;
@@ -756,6 +757,12 @@ __global__ __launch_bounds__(kThreads) void gram_gemm_f32_kernel(GramArgs a, int
 }
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// The float32 paths serve small batches (one image of a few hundred tokens):
+// 128 x 128 tiles would leave most compute units idle, so 64 x 64 tiles are
+// taken while the 128 x 128 ones would not fill the chip once.  Each output
+// accumulates its K in the same order either way.
+inline bool small_f32_tiles(int64_t M, int64_t N) { return ceil_div(M, 128) * ceil_div(N, 128) < 256; }
 
 }  // namespace
 
@@ -803,12 +810,16 @@ hipError_t launch_project_gemm(int dtype, const void* X, int64_t T_vis, const vo
                        proj_blocks, er, wr, T_txt, (int64_t)h, d_text, tproj);
     return hipGetLastError();
   }
-  constexpr int BM = 128, BN = 128, BK = 32;
   ProjRows<float> ar{(const float*)X, T_vis, (const float*)s_start, (const float*)s_stop, d};
   DenseRows<float> br{(const float*)W, d};
-  hipLaunchKernelGGL((project_gemm_kernel<float, float, BM, BN, BK>),
-                     dim3((unsigned)(ceil_div(M, BM) * ceil_div(N, BN))), dim3(kThreads), 0, stream,
-                     ar, br, M, N, d, (float*)out);
+  if (small_f32_tiles(M, N))
+    hipLaunchKernelGGL((project_gemm_kernel<float, float, 64, 64, 32>),
+                       dim3((unsigned)(ceil_div(M, 64) * ceil_div(N, 64))), dim3(kThreads), 0, stream,
+                       ar, br, M, N, d, (float*)out);
+  else
+    hipLaunchKernelGGL((project_gemm_kernel<float, float, 128, 128, 32>),
+                       dim3((unsigned)(ceil_div(M, 128) * ceil_div(N, 128))), dim3(kThreads), 0,
+                       stream, ar, br, M, N, d, (float*)out);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_text_gemm_f32(E, T_txt, W_text, d_text, h, tproj, stream);
@@ -841,11 +852,17 @@ hipError_t launch_gram_gemm(const GramArgs& a, hipStream_t stream) {
   } else {
     hipLaunchKernelGGL(ctx_split_kernel<float>, dim3(a.B), dim3(256), 0, stream, a.ctx, a.h,
                        (float*)a.csplit);
-    const int per_group = (int)(ceil_div(M, 128) * ceil_div(N, 128));
+    const bool small = small_f32_tiles(M * a.G, N);
+    const int T = small ? 64 : 128;
+    const int per_group = (int)(ceil_div(M, T) * ceil_div(N, T));
     const int64_t blocks =
         xcd_grouped ? 8 * ceil_div(a.G, 8) * per_group : (int64_t)a.G * per_group;
-    hipLaunchKernelGGL(gram_gemm_f32_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, a,
-                       per_group, xcd_grouped);
+    if (small)
+      hipLaunchKernelGGL((gram_gemm_f32_kernel<64, 64>), dim3((unsigned)blocks), dim3(kThreads), 0,
+                         stream, a, per_group, xcd_grouped);
+    else
+      hipLaunchKernelGGL((gram_gemm_f32_kernel<128, 128>), dim3((unsigned)blocks), dim3(kThreads), 0,
+                         stream, a, per_group, xcd_grouped);
   }
   return hipGetLastError();
 }

@@ -130,6 +130,10 @@ _add(Workload("mid_bf16", 104, batch=3, d=1024, d_text=1024, h=1024, dtype="bf16
               text_len=40, tokens=(576, 576, 300), cap=192, layout="padded",
               stop_target=("mean_k", 64.0),
               description="hidden 1024 bf16 with full 576-token groups and long caps"))
+_add(Workload("wide_f32", 105, batch=12, d=512, d_text=512, h=256, dtype="f32",
+              text_len=16, tokens=(576,) * 12, cap=64, layout="padded",
+              stop_target=("mean_k", 40.0),
+              description="fp32 batch large enough for the 128 x 128 float32 tiles"))
 
 # Grouped selection, g = 5 tokens per round (the setting of the high-resolution
 # backbones), on the same shapes: small parity cases, then the three
@@ -159,7 +163,7 @@ _add(Workload("internvl3_g5_bf16", 15, batch=64, d=3584, d_text=3584, h=1024, dt
               description="64 images x 13 groups x 256 tokens, d=3584, 5 tokens per round"))
 
 PAPER_WORKLOADS = ["single_f32", "llava15_bf16", "llavanext_bf16", "qwen25vl_bf16", "internvl3_bf16"]
-SMALL_WORKLOADS = ["tiny_f32", "tiny_bf16", "small_packed_bf16", "mid_bf16"]
+SMALL_WORKLOADS = ["tiny_f32", "tiny_bf16", "small_packed_bf16", "mid_bf16", "wide_f32"]
 GROUPED_SMALL_WORKLOADS = ["tiny_g5_f32", "small_g5_bf16", "mid_g5_bf16"]
 GROUPED_WORKLOADS = ["llavanext_g5_bf16", "qwen25vl_g5_bf16", "internvl3_g5_bf16"]
 
