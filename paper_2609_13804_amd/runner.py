@@ -193,6 +193,25 @@ class DeviceRun:
         if self.out is not None:
             self.compact(stream)
 
+    # ---------------------------------------------------------------- graphs
+    def capture(self, stages=("project", "select", "compact")):
+        """A HIP graph of the given stages on this run's buffers (one step by
+        default), replayed with ``g.replay()`` on the current stream.  Every
+        entry point only launches kernels, so a step captures whole; the
+        stages are run once eagerly on the capture stream first."""
+        todo = [getattr(self, st) for st in stages if st != "compact" or self.out is not None]
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for f in todo:
+                f()
+        torch.cuda.current_stream().wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for f in todo:
+                f()
+        return g
+
     def device_errors(self):
         return [sp.stepprune_read_device_error(ws) for ws in self.ws]
 
@@ -279,6 +298,16 @@ class Pipeline:
         self.done = [torch.cuda.Event() for _ in self.runs]
         self.split_gram = split_gram
         self.k = 0
+        self.graphs = None
+
+    def use_graphs(self):
+        """Replay each slot's stages from HIP graphs (the projection, and the
+        selection with compaction) instead of enqueuing their kernels one by
+        one; the streams and events between them stay as they are."""
+        if self.split_gram:
+            raise ValueError("graphs replay whole stages")
+        self.graphs = [(r.capture(("project",)), r.capture(("select", "compact"))) for r in self.runs]
+        torch.cuda.synchronize()
 
     def issue(self):
         """Queue the next batch (nothing waits on the host)."""
@@ -287,6 +316,17 @@ class Pipeline:
         ss = self.sel_streams[self.k % len(self.sel_streams)]
         if self.k >= len(self.runs):
             ps.wait_event(self.done[s])
+        if self.graphs is not None:
+            gp, gs = self.graphs[s]
+            with torch.cuda.stream(ps):
+                gp.replay()
+            self.projected[s].record(ps)
+            ss.wait_event(self.projected[s])
+            with torch.cuda.stream(ss):
+                gs.replay()
+            self.done[s].record(ss)
+            self.k += 1
+            return
         r.project(ps.cuda_stream)
         if self.split_gram:
             r.select(ps.cuda_stream, flags=r.flags | sp.SP_GRAM_ONLY)
