@@ -822,6 +822,8 @@ def main(argv=None):
             note="one workgroup per episode; its time is the longest episode's chain of "
                  "dependent steps, so the FMA-rate fraction says little"),
     }
+    # the plain selection's kept lists, before an optional pass reuses the run
+    plain_kept = run.kept_lists()
     if args.trajectory is not None:
         out["trajectory"] = trajectory_pass(run, args.trajectory, K, hip)
     if args.encoder:
@@ -841,7 +843,7 @@ def main(argv=None):
     steady = args.steady if args.steady >= 0 else (max(1, N_CU // s.G) if s.G < 128 else 0)
     if steady > 0:
         out["select_steady"] = steady_pass(w, steady, b_stop, hip, stream, t_scan_roof,
-                                           run.kept_lists(), max(steps_g))
+                                           plain_kept, max(steps_g))
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, lay, b_stop, args.cpu_budget)
         one = cpu_baseline(w, lay, b_stop, args.cpu_budget * 0.5, single_thread=True)
