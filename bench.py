@@ -111,11 +111,13 @@ def _episode_steps(caps, sizes, kept, g=1):
     return steps
 
 
-def cpu_baseline(w, lay, b_stop, budget_s, single_thread=False):
+def cpu_baseline(w, lay, b_stop, budget_s, single_thread=False, gpu_kept=None):
     """The oracle (float64 NumPy, as written) over a bounded sample of the batch:
     chunks of up to 4 images, passing over the batch again until the oracle has
     run for the time budget.  With single_thread the BLAS pool is limited to
-    one thread (the selection loop is single-threaded Python either way)."""
+    one thread (the selection loop is single-threaded Python either way).
+    With gpu_kept (the GPU's kept lists of the batch) the sampled images'
+    oracle sets are compared with them, outside the timed region."""
     import contextlib
     limit = contextlib.nullcontext()
     try:
@@ -127,10 +129,10 @@ def cpu_baseline(w, lay, b_stop, budget_s, single_thread=False):
     except Exception:
         threads = 1 if single_thread else (os.cpu_count() or 1)
     with limit:
-        return _oracle_sample(w, b_stop, budget_s, threads)
+        return _oracle_sample(w, b_stop, budget_s, threads, gpu_kept)
 
 
-def _oracle_sample(w, b_stop, budget_s, threads):
+def _oracle_sample(w, b_stop, budget_s, threads, gpu_kept=None):
     import numpy as np
     import oracle
     from paper_2609_13804_amd import workloads as W
@@ -140,6 +142,7 @@ def _oracle_sample(w, b_stop, budget_s, threads):
     images = list(range(w.batch))
     chunks = [images[i:i + chunk] for i in range(0, w.batch, chunk)]
     k = 0
+    equal = {}                                 # image -> oracle set == GPU set
     while elapsed < budget_s:
         sub = chunks[k % len(chunks)]
         k += 1
@@ -154,10 +157,20 @@ def _oracle_sample(w, b_stop, budget_s, threads):
                            sl.rows_per_image, np.zeros((sl.out_rows, w.d)))
         elapsed += time.perf_counter() - t0
         done += len(sub)
-    return {"value": done / elapsed, "unit": "images/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{done} images ({done / w.batch:.2f} passes over the {w.batch}-image "
-                      f"{w.name} batch, chunks of {chunk}) of project + select + compact in "
-                      f"float64, {elapsed:.1f} s"}
+        if gpu_kept is not None:
+            for i, b in enumerate(sub):
+                equal[b] = list(res.kept[i]) == list(gpu_kept[b])
+    out = {"value": done / elapsed, "unit": "images/s", "cores": int(threads), "kind": "oracle",
+           "sample": f"{done} images ({done / w.batch:.2f} passes over the {w.batch}-image "
+                     f"{w.name} batch, chunks of {chunk}) of project + select + compact in "
+                     f"float64, {elapsed:.1f} s"}
+    if gpu_kept is not None:
+        out["parity"] = {"images_compared": len(equal), "kept_sets_equal": int(sum(equal.values())),
+                         "how": "the oracle end to end from the raw inputs (its own float64 "
+                                "projection) against the GPU's kept lists of the same images; "
+                                "bfloat16 sets may differ at near-ties that the stored-value "
+                                "rounding flips (the parity tests check each such divergence)"}
+    return out
 
 
 def steady_pass(w, R, b_stop, hip, stream, t_scan_roof, ref_kept, longest, steps=10, warmup=2):
@@ -845,7 +858,7 @@ def main(argv=None):
         out["select_steady"] = steady_pass(w, steady, b_stop, hip, stream, t_scan_roof,
                                            plain_kept, max(steps_g))
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, lay, b_stop, args.cpu_budget)
+        out["cpu_baseline"] = cpu_baseline(w, lay, b_stop, args.cpu_budget, gpu_kept=plain_kept)
         one = cpu_baseline(w, lay, b_stop, args.cpu_budget * 0.5, single_thread=True)
         out["cpu_baseline"]["single_core"] = {"value": one["value"], "unit": one["unit"],
                                               "sample": one["sample"]}
