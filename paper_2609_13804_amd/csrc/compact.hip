@@ -3,7 +3,7 @@
 //
 // Pure data movement, bound by HBM bandwidth: every kept row and every text
 // row is read once and written once with 16-byte vector accesses, one wave per
-// row.  Grid: (row blocks, image).  For the packed layout each workgroup
+// row, all of a row's loads in flight before its stores.  Grid: (row blocks, image).  For the packed layout each workgroup
 // derives its image's start row from the kept counts of the earlier images
 // (cu[b] = text_off[b] - text_off[0] + sum_{b' < b} K_b'), so no separate
 // scan kernel is needed; the first workgroup of each image writes its
@@ -75,8 +75,28 @@ __global__ __launch_bounds__(kCompactWaves * 64) void compact_kernel(CompactArgs
       src = E + (t0 + r - K) * row_bytes;
     }
     char* dst = out + (base + r) * row_bytes;
-    for (int c = lane; c < chunks; c += 64)
-      reinterpret_cast<u32x4_t*>(dst)[c] = reinterpret_cast<const u32x4_t*>(src)[c];
+    // A row's loads are all issued before its stores (eight 16-byte chunks per
+    // lane at a time, 8 KB per wave in flight); load-store pairs through
+    // possibly aliasing pointers would each wait for their own load.  Chunk
+    // indices past the row are clamped to its last chunk rather than skipped:
+    // those lanes copy that chunk again (the same bytes to the same place), and
+    // the loop stays free of branches, whose joins would make the compiler wait
+    // for every access before the next.
+    const u32x4_t* s16 = reinterpret_cast<const u32x4_t*>(src);
+    u32x4_t* d16 = reinterpret_cast<u32x4_t*>(dst);
+    for (int c0 = 0; c0 < chunks; c0 += 8 * 64) {
+      u32x4_t v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int c = c0 + lane + 64 * k;
+        v[k] = s16[c < chunks ? c : chunks - 1];
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int c = c0 + lane + 64 * k;
+        d16[c < chunks ? c : chunks - 1] = v[k];
+      }
+    }
   }
 }
 
