@@ -130,7 +130,7 @@ _add(Workload("mid_bf16", 104, batch=3, d=1024, d_text=1024, h=1024, dtype="bf16
               text_len=40, tokens=(576, 576, 300), cap=192, layout="padded",
               stop_target=("mean_k", 64.0),
               description="hidden 1024 bf16 with full 576-token groups and long caps"))
-_add(Workload("wide_f32", 105, batch=12, d=512, d_text=512, h=256, dtype="f32",
+_add(Workload("wide_f32", 120, batch=12, d=512, d_text=512, h=256, dtype="f32",
               text_len=16, tokens=(576,) * 12, cap=64, layout="padded",
               stop_target=("mean_k", 40.0),
               description="fp32 batch large enough for the 128 x 128 float32 tiles"))
