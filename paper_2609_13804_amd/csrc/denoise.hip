@@ -9,15 +9,16 @@
 // Restricting the block's self-attention to the diagonal gives every token a
 // single key, its own, so the softmax weight is 1 and the attention output is
 // the value projection; the block is per-token work: four dense products on
-// the matrix cores (gemm.hip) and five row kernels here.  The residual stream
+// the matrix cores (gemm.hip; the value bias and the MLP's bias and GELU run
+// in their epilogues) and three row kernels here.  The residual stream
 // (x~, then h) stays float32; every product operand and result is bfloat16,
 // rounded once to nearest-even.
 //
 // Row kernels (row_ops.h for the shared pieces): 16-byte accesses (8 bfloat16
 // or 4 float32 elements); the LayerNorm kernels run one wave per token row and
 // sum in a fixed order (per-lane partial sums, then a butterfly), so results
-// are deterministic.  The bias, bias + GELU and residual + LayerNorm kernels
-// serve the input encoder too (launchers below).
+// are deterministic.  The residual + LayerNorm kernel serves the input
+// encoder too (launcher below).
 #include "sp_internal.h"
 #include "row_ops.h"
 
@@ -77,39 +78,8 @@ __global__ __launch_bounds__(64 * kRowWaves) void resid_ln_kernel(
   ln_store(v, nch, d, lane, g, b, z + r * d);
 }
 
-// The flat passes: one workgroup per row of width n (a multiple of 8), each
+// The flat pass: one workgroup per row of width d (a multiple of 8), each
 // thread taking 8-element chunks.
-//   P = bf16(P + bias)
-__global__ __launch_bounds__(256) void bias_kernel(uint16_t* __restrict__ P, int n,
-                                                   const float* __restrict__ bias) {
-  uint16_t* row = P + (int64_t)blockIdx.x * n;
-  for (int c = 8 * threadIdx.x; c < n; c += 8 * 256) {
-    float x[8], bb[8];
-    load8(row + c, x);
-    load8(bias + c, bb);
-#pragma unroll
-    for (int k = 0; k < 8; ++k) x[k] += bb[k];
-    store8(row + c, x);
-  }
-}
-
-//   H = bf16(GELU(H + b_1)), the exact GELU x Phi(x)
-__global__ __launch_bounds__(256) void bias_gelu_kernel(uint16_t* __restrict__ H, int n,
-                                                        const float* __restrict__ bias) {
-  uint16_t* row = H + (int64_t)blockIdx.x * n;
-  for (int c = 8 * threadIdx.x; c < n; c += 8 * 256) {
-    float x[8], bb[8];
-    load8(row + c, x);
-    load8(bias + c, bb);
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const float y = x[k] + bb[k];
-      x[k] = 0.5f * y * (1.0f + erff(y * 0.70710678118654752f));
-    }
-    store8(row + c, x);
-  }
-}
-
 //   out = bf16((h + t) + b_2)
 __global__ __launch_bounds__(256) void out_kernel(const float* __restrict__ h,
                                                   const uint16_t* __restrict__ t, int d,
@@ -129,20 +99,6 @@ __global__ __launch_bounds__(256) void out_kernel(const float* __restrict__ h,
 
 }  // namespace
 
-hipError_t launch_row_bias(uint16_t* P, int64_t rows, int n, const float* bias,
-                           hipStream_t stream) {
-  if (rows > 0)
-    hipLaunchKernelGGL(bias_kernel, dim3((unsigned)rows), dim3(256), 0, stream, P, n, bias);
-  return hipGetLastError();
-}
-
-hipError_t launch_row_bias_gelu(uint16_t* H, int64_t rows, int n, const float* bias,
-                                hipStream_t stream) {
-  if (rows > 0)
-    hipLaunchKernelGGL(bias_gelu_kernel, dim3((unsigned)rows), dim3(256), 0, stream, H, n, bias);
-  return hipGetLastError();
-}
-
 hipError_t launch_resid_ln(float* xt, const uint16_t* t, const float* bias, int64_t T, int d,
                            const float* g, const float* b, uint16_t* z, hipStream_t stream) {
   if (T > 0)
@@ -161,15 +117,13 @@ hipError_t launch_gate_denoise(const DenoiseArgs& a, hipStream_t stream) {
   hipError_t e;
   hipLaunchKernelGGL(gate_ln_kernel, dim3(rows), dim3(64 * kRowWaves), 0, stream, a.X, a.alpha,
                      a.eps, T, d, a.ln1_g, a.ln1_b, a.xt, P);
-  if ((e = launch_dense_bf16(P, a.W_v, T, d, d, Q, stream)) != hipSuccess) return e;     // W_V z
-  hipLaunchKernelGGL(bias_kernel, dim3((unsigned)T), dim3(256), 0, stream, Q, d, a.b_v);
+  if ((e = launch_dense_bf16(P, a.W_v, T, d, d, Q, stream, a.b_v)) != hipSuccess) return e;  // W_V z + b_V
   if ((e = launch_dense_bf16(Q, a.W_o, T, d, d, P, stream)) != hipSuccess) return e;     // W_O u
   hipLaunchKernelGGL(resid_ln_kernel, dim3(rows), dim3(64 * kRowWaves), 0, stream, a.xt, P,
                      a.b_o, T, d, a.ln2_g, a.ln2_b, Q);
-  if ((e = launch_dense_bf16(Q, a.W_1, T, 4 * (int64_t)d, d, a.hid, stream)) != hipSuccess)
-    return e;                                                                             // W_1 z
-  hipLaunchKernelGGL(bias_gelu_kernel, dim3((unsigned)T), dim3(256), 0, stream, a.hid, 4 * d,
-                     a.b_1);
+  if ((e = launch_dense_bf16(Q, a.W_1, T, 4 * (int64_t)d, d, a.hid, stream, a.b_1, true)) !=
+      hipSuccess)
+    return e;                                                                  // GELU(W_1 z + b_1)
   if ((e = launch_dense_bf16(a.hid, a.W_2, T, d, 4 * d, P, stream)) != hipSuccess) return e;  // W_2 a
   hipLaunchKernelGGL(out_kernel, dim3((unsigned)T), dim3(256), 0, stream, a.xt, P, d, a.b_2,
                      a.out);

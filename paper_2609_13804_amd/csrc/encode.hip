@@ -7,8 +7,9 @@
 // Enc is two pre-norm transformer blocks of width d: multi-head attention with
 // heads of width 128 over the image's whole sequence (bidirectional, or causal
 // on request), and an MLP 4d wide with the exact GELU.  Every linear map runs
-// on the matrix cores (gemm.hip's bfloat16 core); biases, GELU and the
-// residual + LayerNorm steps are row kernels (denoise.hip), the rest is here.
+// on the matrix cores (gemm.hip's bfloat16 core), the q/k/v bias and the MLP's
+// bias and GELU in the products' epilogues; the residual + LayerNorm steps are
+// row kernels (denoise.hip), the rest is here.
 //
 // Sequence layout: image b's sequence occupies rows [so_b, so_b + S_b) of the
 // workspace buffers, so_b = img_off[b] + text_off[b], S_b = N_b + L_b, its
@@ -424,10 +425,10 @@ hipError_t launch_encode(const EncodeArgs& a, hipStream_t stream) {
   const dim3 vt_grid((unsigned)(smax_pad / kVtKeys), (unsigned)heads, (unsigned)a.B);
   for (int k = 0; k < kEncoderBlocks; ++k) {
     const EncoderBlockArgs& p = a.blk[k];
-    // q, k, v of LN1(R) (in L)
-    if ((e = launch_dense_bf16(a.L, p.W_qkv, S, 3 * (int64_t)d, d, a.QKV, stream)) != hipSuccess)
+    // q, k, v of LN1(R) (in L), biased in the product's epilogue
+    if ((e = launch_dense_bf16(a.L, p.W_qkv, S, 3 * (int64_t)d, d, a.QKV, stream, p.b_qkv)) !=
+        hipSuccess)
       return e;
-    if ((e = launch_row_bias(a.QKV, S, 3 * d, p.b_qkv, stream)) != hipSuccess) return e;
     hipLaunchKernelGGL(vt_kernel, vt_grid, dim3(256), 0, stream, a.QKV, d, smax_pad, a.img_off,
                        a.text_off, a.max_seq, S, a.Vt, a.err);
     hipLaunchKernelGGL(attn_kernel, attn_grid, dim3(64 * kAttnWaves), 0, stream, a.QKV, a.Vt, d,
@@ -438,9 +439,9 @@ hipError_t launch_encode(const EncodeArgs& a, hipStream_t stream) {
     if ((e = launch_resid_ln(a.R, a.L, p.b_o, S, d, p.ln2_g, p.ln2_b, a.A, stream)) != hipSuccess)
       return e;
     // the MLP
-    if ((e = launch_dense_bf16(a.A, p.W_1, S, 4 * (int64_t)d, d, a.HID, stream)) != hipSuccess)
+    if ((e = launch_dense_bf16(a.A, p.W_1, S, 4 * (int64_t)d, d, a.HID, stream, p.b_1, true)) !=
+        hipSuccess)
       return e;
-    if ((e = launch_row_bias_gelu(a.HID, S, 4 * d, p.b_1, stream)) != hipSuccess) return e;
     if ((e = launch_dense_bf16(a.HID, p.W_2, S, d, 4 * d, a.L, stream)) != hipSuccess) return e;
     if (k + 1 < kEncoderBlocks) {
       // R += L + b_2, and the next block's LN1 into L (in place, row by row)

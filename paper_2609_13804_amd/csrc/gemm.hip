@@ -194,11 +194,19 @@ __device__ __forceinline__ int swz(int row, int chunk) {
 // WAVES = 4: each wave owns a 128 x 128 quadrant (one wave per SIMD).
 // WAVES = 8: each wave owns 128 x 64 (two waves per SIMD, so one wave's
 // matrix-core work covers the other's waits at barriers and loads).
-template <int WAVES, typename OutT, class ARows, class BRows>
+// Output epilogue of the bfloat16 core: the product as it is, or (bfloat16
+// output only) the product rounded to bfloat16, plus a per-column float32 bias,
+// optionally through the exact GELU, rounded again: the same values as storing
+// the product and then running a bias (+ GELU) pass over it.
+constexpr int kEpiNone = 0, kEpiBias = 1, kEpiBiasGelu = 2;
+
+template <int WAVES, typename OutT, class ARows, class BRows, int EPI = kEpiNone>
 __device__ __forceinline__ void gemm_bf16_256(const ARows& ar, const BRows& br, int64_t M,
                                               int64_t N, int K, OutT* __restrict__ C, int64_t ldc,
-                                              int64_t m0, int64_t n0, char* smem) {
+                                              int64_t m0, int64_t n0, char* smem,
+                                              const float* __restrict__ bias = nullptr) {
   static_assert(WAVES == 4 || WAVES == 8, "four or eight waves");
+  static_assert(EPI == kEpiNone || sizeof(OutT) == 2, "bias epilogues write bfloat16");
   constexpr int GPW = 16 / WAVES;            // 16-row groups per operand per wave
   constexpr int LPW = 2 * GPW;               // DMA instructions per wave per stage
   constexpr int WGN = WAVES / 2;             // waves along N (two along M)
@@ -367,6 +375,12 @@ __device__ __forceinline__ void gemm_bf16_256(const ARows& ar, const BRows& br, 
     if (PASSES == 1 || wm == p) {
       // 32x32 MFMA result layout: lane l, register r holds
       // row 8*(r/4) + 4*(l/32) + r%4, column l%32.
+      float bj[TN];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int64_t col = n0 + wn * (32 * TN) + j * 32 + (lane & 31);
+        bj[j] = EPI != kEpiNone && col < N ? bias[col] : 0.0f;
+      }
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -375,7 +389,15 @@ __device__ __forceinline__ void gemm_bf16_256(const ARows& ar, const BRows& br, 
           for (int r = 0; r < 16; ++r) {
             const int lr = wm * 128 - p * ROWS + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
             const int lc = wn * (32 * TN) + j * 32 + (lane & 31);
-            T[lr * kBN + ((lc / EPC) ^ sw(lr)) * EPC + lc % EPC] = store_cvt<OutT>(acc[i][j][r]);
+            OutT v;
+            if constexpr (EPI == kEpiNone) {
+              v = store_cvt<OutT>(acc[i][j][r]);
+            } else {
+              float y = __uint_as_float((uint32_t)f32_to_bf16_rne(acc[i][j][r]) << 16) + bj[j];
+              if constexpr (EPI == kEpiBiasGelu) y = 0.5f * y * (1.0f + erff(y * 0.70710678118654752f));
+              v = f32_to_bf16_rne(y);
+            }
+            T[lr * kBN + ((lc / EPC) ^ sw(lr)) * EPC + lc % EPC] = v;
           }
     }
     __syncthreads();
@@ -496,17 +518,19 @@ __global__ __launch_bounds__(64 * kProjWaves) void project_gemm_bf16_kernel(
   }
 }
 
-// A plain bfloat16 product C = A B^T (bfloat16 out) on the 256 x 256 core,
-// tiles in XCD-grouped order.
+// A bfloat16 product C = A B^T (bfloat16 out) on the 256 x 256 core, tiles in
+// XCD-grouped order, with an optional bias (+ GELU) epilogue.
+template <int EPI>
 __global__ __launch_bounds__(64 * kProjWaves) void dense_bf16_kernel(DenseRows<__bf16> ar,
                                                                     DenseRows<__bf16> br,
                                                                     int64_t M, int64_t N, int K,
-                                                                    uint16_t* C) {
+                                                                    uint16_t* C, const float* bias) {
   __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes];
   const int64_t nt = (N + kBN - 1) / kBN;
   const int64_t t = xcd_tile(blockIdx.x, ((M + kBM - 1) / kBM) * nt);
   if (t < 0) return;
-  gemm_bf16_256<kProjWaves, uint16_t>(ar, br, M, N, K, C, N, (t / nt) * kBM, (t % nt) * kBN, smem);
+  gemm_bf16_256<kProjWaves, uint16_t, DenseRows<__bf16>, DenseRows<__bf16>, EPI>(
+      ar, br, M, N, K, C, N, (t / nt) * kBM, (t % nt) * kBN, smem, bias);
 }
 
 // grid.x: output tiles, grid.y: K split p, which covers k in [p K, (p + 1) K)
@@ -868,13 +892,20 @@ hipError_t launch_gram_gemm(const GramArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_dense_bf16(const void* A, const void* B, int64_t M, int64_t N, int K, void* C,
-                             hipStream_t stream) {
+                             hipStream_t stream, const float* bias, bool gelu) {
   if (M == 0 || N == 0) return hipSuccess;
   DenseRows<__bf16> ar{(const __bf16*)A, K};
   DenseRows<__bf16> br{(const __bf16*)B, K};
-  const int64_t blocks = ceil_div(ceil_div(M, kBM) * ceil_div(N, kBN), 8) * 8;
-  hipLaunchKernelGGL(dense_bf16_kernel, dim3((unsigned)blocks), dim3(64 * kProjWaves), 0, stream,
-                     ar, br, M, N, K, (uint16_t*)C);
+  const dim3 grid((unsigned)(ceil_div(ceil_div(M, kBM) * ceil_div(N, kBN), 8) * 8));
+  const dim3 block(64 * kProjWaves);
+  uint16_t* out = (uint16_t*)C;
+  if (!bias)
+    hipLaunchKernelGGL(dense_bf16_kernel<kEpiNone>, grid, block, 0, stream, ar, br, M, N, K, out, bias);
+  else if (!gelu)
+    hipLaunchKernelGGL(dense_bf16_kernel<kEpiBias>, grid, block, 0, stream, ar, br, M, N, K, out, bias);
+  else
+    hipLaunchKernelGGL(dense_bf16_kernel<kEpiBiasGelu>, grid, block, 0, stream, ar, br, M, N, K, out,
+                       bias);
   return hipGetLastError();
 }
 

@@ -148,9 +148,11 @@ struct CompactArgs {
 hipError_t launch_compact(const CompactArgs& a, hipStream_t stream);
 
 // C = A B^T for bfloat16 A [M, K] and B [N, K] (rows K-contiguous), bfloat16
-// C [M, N]; K a multiple of 32.
+// C [M, N]; K a multiple of 32.  With bias [N] (float32) each element is
+// bf16(bf16(product) + bias), or bf16(GELU(bf16(product) + bias)) with gelu:
+// what a separate bias (+ GELU) pass over the stored product gives.
 hipError_t launch_dense_bf16(const void* A, const void* B, int64_t M, int64_t N, int K, void* C,
-                             hipStream_t stream);
+                             hipStream_t stream, const float* bias = nullptr, bool gelu = false);
 
 // Noise gate and locally masked denoiser (denoise.hip).  Workspace buffers:
 // xt float32 [T, d] (the residual stream), buf_p and buf_q bfloat16 [T, d],
@@ -183,14 +185,8 @@ struct DenoiseArgs {
 };
 hipError_t launch_gate_denoise(const DenoiseArgs& a, hipStream_t stream);
 
-// Row kernels of denoise.hip, shared with the encoder:
-//   P = bf16(P + bias) and H = bf16(GELU(H + bias)) over rows of width n;
-//   xt = (xt + t) + bias in place and z = LN(xt) (scale g, shift b) over rows
-//   of width d (d <= 4096).
-hipError_t launch_row_bias(uint16_t* P, int64_t rows, int n, const float* bias,
-                           hipStream_t stream);
-hipError_t launch_row_bias_gelu(uint16_t* H, int64_t rows, int n, const float* bias,
-                                hipStream_t stream);
+// Row kernel of denoise.hip, shared with the encoder: xt = (xt + t) + bias in
+// place and z = LN(xt) (scale g, shift b) over rows of width d (d <= 4096).
 hipError_t launch_resid_ln(float* xt, const uint16_t* t, const float* bias, int64_t T, int d,
                            const float* g, const float* b, uint16_t* z, hipStream_t stream);
 
