@@ -418,13 +418,23 @@ __device__ __forceinline__ void gemm_bf16_256(const ARows& ar, const BRows& br, 
   }
 }
 
-// Workgroup w runs on XCD w % 8; give each XCD a contiguous run of tiles (in
-// N-fastest order) so that tiles sharing an A panel run side by side and share
-// that XCD's L2.  Returns -1 for the padding workgroups of the last run.
-__device__ __forceinline__ int64_t xcd_tile(int64_t w, int64_t tiles) {
+// Workgroup w runs on XCD w % 8, which takes a contiguous run of the tiles in
+// banded order: bands of kBand row panels, each band walked column by column
+// (the last band as tall as the rows left).  The 32 tiles one XCD runs at a
+// time then cover about kBand row panels and 32 / kBand column panels, so they
+// share about 12 operand panels in that XCD's L2 (a row-major run of 32 tiles
+// spans all the column panels of a wide product).  Returns -1 for the padding
+// workgroups of the last run.
+constexpr int64_t kBand = 4;
+
+__device__ __forceinline__ int64_t xcd_tile(int64_t w, int64_t mt, int64_t nt) {
+  const int64_t tiles = mt * nt;
   const int64_t per = (tiles + 7) / 8;
-  const int64_t t = (w % 8) * per + w / 8;
-  return t < tiles ? t : -1;
+  const int64_t i = (w % 8) * per + w / 8;
+  if (i >= tiles) return -1;
+  const int64_t band = i / (kBand * nt), o = i % (kBand * nt);
+  const int64_t rows = mt - band * kBand < kBand ? mt - band * kBand : kBand;
+  return (band * kBand + o % rows) * nt + o / rows;
 }
 
 // ------------------------------------------------------------------ row maps
@@ -506,8 +516,7 @@ __global__ __launch_bounds__(64 * kProjWaves) void project_gemm_bf16_kernel(
   __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes];
   if ((int64_t)blockIdx.x < proj_blocks) {
     const int64_t nt = (N + kBN - 1) / kBN;
-    const int64_t tiles = ((M + kBM - 1) / kBM) * nt;
-    const int64_t t = xcd_tile(blockIdx.x, tiles);
+    const int64_t t = xcd_tile(blockIdx.x, (M + kBM - 1) / kBM, nt);
     if (t < 0) return;
     gemm_bf16_256<kProjWaves, uint16_t>(ar, br, M, N, K, C, N, (t / nt) * kBM, (t % nt) * kBN, smem);
   } else {
@@ -527,7 +536,7 @@ __global__ __launch_bounds__(64 * kProjWaves) void dense_bf16_kernel(DenseRows<_
                                                                     uint16_t* C, const float* bias) {
   __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes];
   const int64_t nt = (N + kBN - 1) / kBN;
-  const int64_t t = xcd_tile(blockIdx.x, ((M + kBM - 1) / kBM) * nt);
+  const int64_t t = xcd_tile(blockIdx.x, (M + kBM - 1) / kBM, nt);
   if (t < 0) return;
   gemm_bf16_256<kProjWaves, uint16_t, DenseRows<__bf16>, DenseRows<__bf16>, EPI>(
       ar, br, M, N, K, C, N, (t / nt) * kBM, (t % nt) * kBN, smem, bias);
