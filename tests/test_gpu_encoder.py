@@ -4,8 +4,9 @@ the oracle (oracle/encoder.py), through the C ABI.
 Small batches are checked on every row of H, with ragged sequences (lengths
 that are not multiples of the 32-key blocks, more than one 128-query block,
 an image without text, an image with one visual token), both attention
-directions and two widths; the 16 x 640-token batch at d = 4096 is checked on
-two whole images.
+directions and three widths (at d = 384 the q/k/v product's columns end in
+a partial tile, so its bias epilogue runs on a ragged edge); the 16 x
+640-token batch at d = 4096 is checked on two whole images.
 
 Tolerance.  The oracle's exact mode is the definition; its mirror mode rounds
 to bfloat16 where the GPU stores bfloat16.  Per row of H the GPU must be within
@@ -111,6 +112,8 @@ SMALL = [
     # (name, seed, d, d_text, visual tokens per image, text tokens per image)
     ("ragged_d256", 1, 256, 192, (70, 33, 200, 1), (5, 0, 12, 40)),
     ("d512", 2, 512, 256, (129, 64, 17), (31, 64, 3)),
+    # three heads: the q/k/v product's 1152 columns end in half a 256-column tile
+    ("d384", 3, 384, 128, (90, 300), (20, 7)),
 ]
 
 
