@@ -693,6 +693,50 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     const float inv = GROUPED ? sm[0] : s_inv, st = GROUPED ? sm[1] : s_st;
     const float e_new = GROUPED ? 0.0f : s_enew;
 
+    // ---- second columns (waves 0-3), older entries: each lane sums its
+    // quarter of every 16-entry block, 64 entries per pass with all eight
+    // reads issued first, and a quad sum combines the quarters.  Entries past
+    // the newest are zero in LDS and alpha is zero past the history, so whole
+    // passes need no masking.  This runs before the lane-owned logits: its LDS
+    // round trips then overlap the other wave of the SIMD (waves 4-7 have no
+    // second columns) instead of holding the step's decision after it.
+    float qs = 0.0f;
+    if (swave) {
+      float acc2 = 0.0f, acc2b = 0.0f;
+      const int last = hl - ng;                // the newest entries are added after the logits
+      const int lend = last < ks ? last : ks;
+      const int st4 = opaque(tid);                 // 4 scl + sq in waves 0-3
+      const float* as = alphaw + 4 * (st4 & 3);
+      const float* hs = hsec + st4 * 4;
+      for (int k0 = 0; 16 * k0 < lend; k0 += 4) {
+        float4 av[4], hv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          av[u] = *reinterpret_cast<const float4*>(as + 16 * (k0 + u));
+          hv[u] = *reinterpret_cast<const float4*>(hs + (k0 + u) * 1024);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          acc2 = fmaf(av[u].x, hv[u].x, acc2);
+          acc2b = fmaf(av[u].y, hv[u].y, acc2b);
+          acc2 = fmaf(av[u].z, hv[u].z, acc2);
+          acc2b = fmaf(av[u].w, hv[u].w, acc2b);
+        }
+      }
+      // entries past the LDS tier: read again from the Gram buffer, every
+      // fourth one per lane
+      for (int tau = ks + sq; tau < last; tau += 4) {
+        const int c = hcol[tau];
+        const float hv = scol ? Bm[(int64_t)(c == n + 1 ? n : c) * ld + js] : 0.0f;
+        acc2 = fmaf(alphaw[tau], hv, acc2);
+      }
+      // quad sum of the four quarters: (q0 + q1) + (q2 + q3) in every lane of
+      // the quad (each addition is commutative, so all four agree bit for bit)
+      qs = acc2 + acc2b;
+      qs += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(qs), 0xB1, 0xF, 0xF, true));
+      qs += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(qs), 0x4E, 0xF, 0xF, true));
+    }
+
     // ---- logits of the lane-owned columns: older entries from the history
     // tiers (the newest entry's slots still hold zero), then the newest.
     float acc = 0.0f, accb = 0.0f;   // two independent chains (even, odd entries)
@@ -787,45 +831,9 @@ __global__ __launch_bounds__(MAXT) void select_kernel(SelParams p) {
     const float lj = sigma * (ck_main + a_main + acc * inv);
     const float l_stop = sigma * (ck_stop + a_stop + sp * inv) + p.b_stop;
 
-    // ---- second columns (waves 0-3): each lane sums its quarter of every
-    // 16-entry block, 64 entries per pass with all eight reads issued first.
-    // Entries past the newest are zero in LDS and alpha is zero past the
-    // history, so whole passes need no masking.
+    // ---- second columns: the newest entries, then the logit
     float ls = -INFINITY;
     if (swave) {
-      float acc2 = 0.0f, acc2b = 0.0f;
-      const int last = hl - ng;                // the newest entries are added below
-      const int lend = last < ks ? last : ks;
-      const int st4 = opaque(tid);                 // 4 scl + sq in waves 0-3
-      const float* as = alphaw + 4 * (st4 & 3);
-      const float* hs = hsec + st4 * 4;
-      for (int k0 = 0; 16 * k0 < lend; k0 += 4) {
-        float4 av[4], hv[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          av[u] = *reinterpret_cast<const float4*>(as + 16 * (k0 + u));
-          hv[u] = *reinterpret_cast<const float4*>(hs + (k0 + u) * 1024);
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          acc2 = fmaf(av[u].x, hv[u].x, acc2);
-          acc2b = fmaf(av[u].y, hv[u].y, acc2b);
-          acc2 = fmaf(av[u].z, hv[u].z, acc2);
-          acc2b = fmaf(av[u].w, hv[u].w, acc2b);
-        }
-      }
-      // entries past the LDS tier: read again from the Gram buffer, every
-      // fourth one per lane
-      for (int tau = ks + sq; tau < last; tau += 4) {
-        const int c = hcol[tau];
-        const float hv = scol ? Bm[(int64_t)(c == n + 1 ? n : c) * ld + js] : 0.0f;
-        acc2 = fmaf(alphaw[tau], hv, acc2);
-      }
-      // quad sum of the four quarters: (q0 + q1) + (q2 + q3) in every lane of
-      // the quad (each addition is commutative, so all four agree bit for bit)
-      float qs = acc2 + acc2b;
-      qs += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(qs), 0xB1, 0xF, 0xF, true));
-      qs += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(qs), 0x4E, 0xF, 0xF, true));
       if constexpr (GROUPED) {
 #pragma unroll
         for (int i = 0; i < GMAX; ++i)
