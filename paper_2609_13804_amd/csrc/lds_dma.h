@@ -16,7 +16,10 @@ typedef __attribute__((address_space(3))) void* lptr_t;
 // then waits for every outstanding LDS read (lgkmcnt(0)) wherever a fragment
 // is consumed, including reads issued just before.  The caller awaits its
 // completion explicitly (wait_vmcnt, then a barrier) before any wave reads
-// what it filled.
+// what it filled.  The statement sets M0 itself, right before its load.  The
+// compiler reserves M0 and does not preserve it across inline assembly, so the
+// kernels that use this must not hold any other value in M0; in the generated
+// code every write of M0 is this statement's (tests/test_codegen.py checks it).
 __device__ __forceinline__ void lds_dma16(const void* src, char* dst) {
   const uint32_t l = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lptr_t)dst);
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
