@@ -291,6 +291,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_kernel(
   // key (masked below); V^T keys past the sequence are zero in Vt up to
   // smax_pad.
   static_assert(kKeyTile * kHead * 2 / 1024 == 4 * kAttnWaves, "four row groups per wave");
+  static_assert(kVtKeys % kKeyTile == 0, "V^T rows are padded to whole key tiles");
   auto issue_tile = [&](int kt, int buf) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
