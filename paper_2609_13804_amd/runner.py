@@ -31,6 +31,13 @@ class Sizes:
     kept_total: int
 
 
+def _storage_rows(a: np.ndarray) -> np.ndarray:
+    """The text rows as uploaded: a batch without text still gets one zero row
+    of storage, because the ABI takes a valid E_text pointer (no kernel reads
+    a row outside the ones text_off spans)."""
+    return a if a.shape[0] > 0 else np.zeros((1,) + a.shape[1:], a.dtype)
+
+
 class DeviceRun:
     """All inputs, outputs and workspaces of one batch, resident on the GPU."""
 
@@ -55,7 +62,7 @@ class DeviceRun:
         up = lambda a, dt=tdt: torch.from_numpy(np.ascontiguousarray(a)).to(device=dev, dtype=dt)
         upi = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
         self.X = up(inputs["X"])
-        self.E = up(inputs["E_text"])
+        self.E = up(_storage_rows(inputs["E_text"]))
         self.W_kqv = up(inputs["W_kqv"])
         self.W_text = up(inputs["W_text"])
         self.s_start = up(inputs["s_start"])
@@ -126,11 +133,11 @@ class DeviceRun:
         if inputs is not None:
             up = lambda a, ref: torch.from_numpy(np.ascontiguousarray(a)).to(device=ref.device,
                                                                              dtype=ref.dtype)
-            if inputs["X"].shape != tuple(self.X.shape) or \
-                    inputs["E_text"].shape != tuple(self.E.shape):
+            E = _storage_rows(inputs["E_text"])
+            if inputs["X"].shape != tuple(self.X.shape) or E.shape != tuple(self.E.shape):
                 raise ValueError("a sibling's batch must have the same shape")
             other.X = up(inputs["X"], self.X)
-            other.E = up(inputs["E_text"], self.E)
+            other.E = up(E, self.E)
         other._alloc_outputs()
         return other
 

@@ -326,6 +326,47 @@ def test_images_without_groups(gpu_lib):
     assert run0.kept_cnt.cpu().numpy().tolist() == [0, 0]
 
 
+@pytest.mark.parametrize("dtype,layout", [("bf16", "padded"), ("f32", "packed")])
+def test_batch_without_text(gpu_lib, dtype, layout):
+    """No text token in the batch (T_txt = 0): no text tile or LayerNorm runs,
+    every context is zero (the pooled mean over an empty set, as the oracle
+    defines it), and the projection, the selection and the prefill buffer
+    (visual rows only) match the oracle.  The STOP bias keeps about half of
+    what the caps allow, placed by the oracle's calibration."""
+    from paper_2609_13804_amd.runner import DeviceRun
+    w = W.Workload(f"no_text_{dtype}", 111 if dtype == "bf16" else 112, batch=3, d=256,
+                   d_text=256, h=128, dtype=dtype, text_len=0, tokens=(200, 37, 150), cap=30,
+                   layout=layout, description="no text tokens")
+    lay, inp = W.make_layout(w), W.make_inputs(w)
+    assert int(lay.text_off[-1]) == 0 and inp["E_text"].shape[0] == 0
+    KQV_or = oracle.project(inp["X"], inp["s_start"], inp["s_stop"], inp["W_kqv"], w.dtype)
+    ctx_or = oracle.text_context(inp["E_text"], lay.text_off, inp["W_text"])
+    assert not ctx_or.any()
+    pm = oracle.stop_thresholds(KQV_or, ctx_or, lay.grp_off, lay.grp_img, lay.grp_cap, w.h)
+    b_stop, _ = oracle.choose_stop_bias(pm, 0.5 * sum(len(x) for x in pm))
+    steps = int(max(min(int(c), int(n)) for c, n in zip(lay.grp_cap, np.diff(lay.grp_off)))) + 1
+    run = DeviceRun(w, inp, lay, b_stop, trace_steps=steps, logits=True)
+    run.run()
+    torch.cuda.synchronize()
+    _check_errors(run)
+    KQV, ctx = _staged(run)
+    assert not ctx.any()
+    assert parity.rows_relerr(KQV, KQV_or) <= (1e-3 if dtype == "bf16" else 1e-5)
+    actions = run.trace_actions()
+    rep = parity.check_selection(KQV, ctx, lay.grp_off, lay.grp_img, run.caps_host, run.b_stop, w.h,
+                                 actions, run.trace.cpu().numpy(), w.dtype, logits=_logits(run))
+    kept = run.kept_lists()
+    assert kept == parity.kept_from_actions(actions, lay.grp_off, lay.grp_img, lay.img_off, lay.batch)
+    assert 0 < sum(map(len, kept)) < int(lay.img_off[-1])
+    out_gpu = run.out.float().cpu().numpy()
+    out_or, seq_or = oracle.compact(inp["X"], lay.img_off, inp["E_text"], lay.text_off, kept,
+                                    w.layout, lay.rows_per_image, np.zeros_like(out_gpu))
+    assert np.array_equal(out_gpu, out_or.astype(np.float32))
+    assert run.seq_info.cpu().numpy().tolist() == seq_or.tolist()
+    print(f"no text ({dtype}, {layout}): {rep.episodes} episodes, {rep.steps} steps, kept "
+          f"{[len(k) for k in kept]}", flush=True)
+
+
 def test_device_error_on_oversized_group(gpu_lib):
     """A group larger than the stated max_group is reported through the device
     error word and no kernel reads past its buffers."""
