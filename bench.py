@@ -28,7 +28,7 @@ traffic from the committed counter summary; "measured_peaks" adds rates this
 GPU reaches on library work; "cpu_baseline" is the float64 oracle timed on this
 host's cores over a bounded sample of the same batch.
 
-    python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--streams 3] [--slots 4]
+    python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--streams 3] [--slots 6]
                     [--workload llava15_bf16] [--trajectory TAU BETA] [--steady R] [--denoise]
                     [--encoder] [--lds-probe] [--shared-inputs]
 """
@@ -517,7 +517,7 @@ def main(argv=None):
     ap.add_argument("--hw-queues", type=int, default=0,
                     help="set GPU_MAX_HW_QUEUES (at most 32) for this process before HIP starts, "
                          "to run more pipelined streams on queues of their own (0: leave it)")
-    ap.add_argument("--slots", type=int, default=4,
+    ap.add_argument("--slots", type=int, default=6,
                     help="buffer slots of the staggered pipelined pass (batches in flight)")
     ap.add_argument("--schedule", choices=["staggered", "staggered-gram", "rr"], default="staggered",
                     help="pipelined pass: projections on one stream ahead of select (Gram "
