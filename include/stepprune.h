@@ -304,7 +304,9 @@ sp_status stepprune_select_trajectory(const sp_dims* dims,
 
 /*
  * Algorithm 1 step 5.  Gathers each image's kept visual rows (ascending) and
- * then its text rows into the prefill buffer.  Requires d_text == d.
+ * then its text rows into the prefill buffer.  Requires d_text == d.  X and
+ * E_text must be valid device pointers even when the batch holds no visual or
+ * no text row (the offsets are device data; nothing is read past them).
  *
  *  layout SP_LAYOUT_PADDED: image b owns out rows [b*rows_per_image,
  *         (b+1)*rows_per_image); rows past K_b + L_b are left untouched;
